@@ -1,0 +1,988 @@
+// C-ABI implementation: workspace layout, weight packing, decode-step state machine.
+//
+// One decode step of DVI (Section 3.3) is dvi_draft -> dvi_verify -> dvi_commit; the drafter
+// update (Section 3.4) is dvi_update_drafter.  All device work is enqueued on the context's
+// stream; host bookkeeping (lengths, ring occupancy) mirrors the device so capacity and state
+// errors are caught before anything is launched.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <vector>
+
+#include "../../include/dvi.h"
+#include "kernels.h"
+
+using namespace dvi;
+
+namespace {
+
+constexpr int kMaxRows = 64;   // tokens per GEMM call (four 16-wide MFMA groups)
+constexpr int kChunk = 64;     // attention key chunk
+
+enum State { S_CREATED = 0, S_READY, S_DRAFTED, S_VERIFIED };
+
+struct LayerW {
+    void *wqkv, *wo, *wgu, *wd;
+    float *attn_norm, *mlp_norm;
+    void *Kc, *Vc;
+};
+
+// Bump allocator over the workspace (or a size counter when base == nullptr).
+struct Bump {
+    uint8_t *base;
+    size_t off = 0;
+    explicit Bump(void *b) : base((uint8_t *)b) {}
+    template <class P>
+    P *take(size_t bytes) {
+        off = (off + 255) & ~(size_t)255;
+        P *p = base ? (P *)(base + off) : nullptr;
+        off += bytes;
+        return p;
+    }
+};
+
+}  // namespace
+
+struct dvi_ctx {
+    dvi_config cfg;
+    DType dt;
+    size_t es;
+    hipStream_t stream;
+    std::vector<LayerW> L;
+    void *emb, *head;
+    float *final_norm;
+    float2 *rope;
+    float *lora_A, *lora_B;
+    // activations
+    float *h, *q, *hk, *vlogits, *dlogits, *part_val, *att_po, *att_pml, *lora_u;
+    void *xn, *attn_o, *act, *hk_hat;
+    int32_t *part_idx;
+    // small device state; io block is one contiguous region copied back at commit
+    int32_t *lens, *pending, *drafts, *targets, *forced, *max_new, *ids, *copy_list, *ring_state;
+    int32_t *io;  // [0,B*k) tokens | [B*k, B*k+B) n | [.., +B) m | flags[4]
+    int32_t *prow;
+    // replay ring
+    void *ring_h;
+    float *ring_logits;
+    int32_t *ring_a, *ring_i, *ring_prev;
+    int8_t *ring_r, *ring_fresh;
+    // update
+    float *upd_Z, *upd_stats, *upd_dA, *upd_du, *upd_dB, *upd_loss, *upd_u;
+    float *mA, *vA, *mB, *vB;
+    // host mirror
+    int state = S_CREATED;
+    int B = 0, k_spec = 0, ar_mode = 0;
+    int chunk_stride = 0;
+    std::vector<int32_t> lens_h;
+    int ring_valid_h = 0;
+    bool device_error = false;
+    char err[512] = {0};
+    hipEvent_t ev[8];
+    bool ev_ok = false;
+    float ms[4] = {0, 0, 0, 0};
+    int ev_pending[4] = {0, 0, 0, 0};
+    // kernel probe
+    int probe = 0;
+    std::vector<hipEvent_t> pev;
+    size_t pused = 0;
+    int64_t plaunch = 0;
+    double pbytes = 0.0;
+};
+
+static dvi_status fail(dvi_ctx *c, dvi_status s, const char *fmt, ...) {
+    if (c) {
+        va_list ap;
+        va_start(ap, fmt);
+        vsnprintf(c->err, sizeof(c->err), fmt, ap);
+        va_end(ap);
+        if (s == DVI_ERR_DEVICE) c->device_error = true;
+    }
+    return s;
+}
+
+#define HIPCHK(ctx, expr)                                                                           \
+    do {                                                                                            \
+        hipError_t e_ = (expr);                                                                     \
+        if (e_ != hipSuccess) return fail(ctx, DVI_ERR_DEVICE, "%s: %s", #expr, hipGetErrorString(e_)); \
+    } while (0)
+
+#define LAUNCHCHK(ctx)                                                                              \
+    do {                                                                                            \
+        hipError_t e_ = hipGetLastError();                                                          \
+        if (e_ != hipSuccess) return fail(ctx, DVI_ERR_DEVICE, "kernel launch: %s", hipGetErrorString(e_)); \
+    } while (0)
+
+static size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
+
+static int qkv_rows(const dvi_config &c) { return (c.n_heads + 2 * c.n_kv_heads) * c.head_dim; }
+static int m_max(const dvi_config &c) {
+    int m = c.max_batch * c.max_k_spec;
+    return m > kMaxRows ? m : kMaxRows;
+}
+
+// Lay out (or size, when base == nullptr) everything the context keeps on the device.
+static size_t layout(dvi_ctx *x, const dvi_config &c, void *base) {
+    Bump b(base);
+    const size_t es = c.dtype == DVI_BF16 ? 2 : 4;
+    const size_t d = c.d_model, F = c.ffn_dim, V = c.vocab, qd = (size_t)c.n_heads * c.head_dim;
+    const size_t kvd = (size_t)c.n_kv_heads * c.head_dim;
+    const size_t M = m_max(c), R = c.buffer_rows, r = c.lora_rank;
+    const size_t Bk = (size_t)c.max_batch * c.max_k_spec;
+    const size_t cs = (c.max_seq + kChunk - 1) / kChunk;
+    const size_t cache = (size_t)c.max_batch * kvd * c.max_seq * es;
+    std::vector<LayerW> Ls(c.n_layers);
+    for (int l = 0; l < c.n_layers; ++l) {
+        Ls[l].wqkv = b.take<void>((size_t)qkv_rows(c) * d * es);
+        Ls[l].wo = b.take<void>(d * qd * es);
+        Ls[l].wgu = b.take<void>(2 * F * d * es);
+        Ls[l].wd = b.take<void>(d * F * es);
+        Ls[l].attn_norm = b.take<float>(d * 4);
+        Ls[l].mlp_norm = b.take<float>(d * 4);
+        Ls[l].Kc = b.take<void>(cache);
+        Ls[l].Vc = b.take<void>(cache);
+    }
+    void *emb = b.take<void>(V * d * es);
+    void *head = b.take<void>(V * d * es);
+    float *final_norm = b.take<float>(d * 4);
+    float2 *rope = b.take<float2>((size_t)c.max_seq * (c.head_dim / 2) * 8);
+    float *h = b.take<float>(M * d * 4);
+    void *xn = b.take<void>(M * d * es);
+    float *q = b.take<float>(M * qd * 4);
+    void *attn_o = b.take<void>(M * qd * es);
+    void *act = b.take<void>(M * F * es);
+    float *hk = b.take<float>(Bk * d * 4);
+    void *hk_hat = b.take<void>(Bk * d * es);
+    float *vlogits = b.take<float>(M * V * 4);
+    float *dlogits = b.take<float>((size_t)c.max_batch * V * 4);
+    float *part_val = b.take<float>(M * (V / 16) * 4);
+    int32_t *part_idx = b.take<int32_t>(M * (V / 16) * 4);
+    float *att_po = b.take<float>(M * c.n_heads * cs * c.head_dim * 4);
+    float *att_pml = b.take<float>(M * c.n_heads * cs * 2 * 4);
+    float *lora_u = b.take<float>((M > R ? M : R) * r * 4);
+    int32_t *lens = b.take<int32_t>(c.max_batch * 4);
+    int32_t *pending = b.take<int32_t>(c.max_batch * 4);
+    int32_t *drafts = b.take<int32_t>(Bk * 4);
+    int32_t *targets = b.take<int32_t>(Bk * 4);
+    int32_t *forced = b.take<int32_t>(Bk * 4);
+    int32_t *max_new = b.take<int32_t>(c.max_batch * 4);
+    int32_t *ids = b.take<int32_t>((size_t)c.max_batch * c.max_seq * 4);
+    int32_t *copy_list = b.take<int32_t>((1 + 2 * Bk) * 4);
+    int32_t *ring_state = b.take<int32_t>(4 * 4);
+    int32_t *io = b.take<int32_t>((Bk + 2 * c.max_batch + 4) * 4);
+    size_t maxN = V;
+    if ((size_t)qkv_rows(c) > maxN) maxN = qkv_rows(c);
+    if (2 * F > maxN) maxN = 2 * F;
+    int32_t *prow = b.take<int32_t>(maxN * 4);
+    void *ring_h = b.take<void>(R * d * es);
+    float *ring_logits = b.take<float>(R * V * 4);
+    int32_t *ring_a = b.take<int32_t>(R * 4);
+    int32_t *ring_i = b.take<int32_t>(R * 4);
+    int32_t *ring_prev = b.take<int32_t>(R * 4);
+    int8_t *ring_r = b.take<int8_t>(R);
+    int8_t *ring_fresh = b.take<int8_t>(R);
+    float *upd_Z = b.take<float>(R * V * 4);
+    float *upd_stats = b.take<float>(R * 8 * 4);
+    float *upd_dA = b.take<float>(V * r * 4);
+    float *upd_du = b.take<float>(R * r * 4);
+    float *upd_dB = b.take<float>(r * d * 4);
+    float *upd_loss = b.take<float>(16 * 4);
+    float *mA = b.take<float>(V * r * 4);
+    float *vA = b.take<float>(V * r * 4);
+    float *mB = b.take<float>(r * d * 4);
+    float *vB = b.take<float>(r * d * 4);
+    if (x && base) {
+        x->L = Ls;
+        x->emb = emb; x->head = head; x->final_norm = final_norm; x->rope = rope;
+        x->h = h; x->xn = xn; x->q = q; x->attn_o = attn_o; x->act = act; x->hk = hk; x->hk_hat = hk_hat;
+        x->vlogits = vlogits; x->dlogits = dlogits; x->part_val = part_val; x->part_idx = part_idx;
+        x->att_po = att_po; x->att_pml = att_pml; x->lora_u = lora_u;
+        x->lens = lens; x->pending = pending; x->drafts = drafts; x->targets = targets; x->forced = forced;
+        x->max_new = max_new; x->ids = ids; x->copy_list = copy_list; x->ring_state = ring_state; x->io = io;
+        x->prow = prow;
+        x->ring_h = ring_h; x->ring_logits = ring_logits; x->ring_a = ring_a; x->ring_i = ring_i;
+        x->ring_prev = ring_prev; x->ring_r = ring_r; x->ring_fresh = ring_fresh;
+        x->upd_Z = upd_Z; x->upd_stats = upd_stats; x->upd_dA = upd_dA; x->upd_du = upd_du; x->upd_dB = upd_dB;
+        x->upd_loss = upd_loss; x->upd_u = lora_u;
+        x->mA = mA; x->vA = vA; x->mB = mB; x->vB = vB;
+        x->chunk_stride = (int)cs;
+    }
+    return align_up(b.off);
+}
+
+static const char *check_config(const dvi_config *c) {
+    if (!c) return "null config";
+    if (c->dtype != DVI_FP32 && c->dtype != DVI_BF16) return "dtype must be DVI_FP32 or DVI_BF16";
+    const int kc = c->dtype == DVI_BF16 ? 32 : 16;
+    if (c->n_layers < 1) return "n_layers < 1";
+    if (c->split_k < 1 || c->split_k > c->n_layers) return "split_k must be in [1, n_layers]";
+    if (c->d_model <= 0 || c->d_model % kc) return "d_model must be a positive multiple of 32 (bf16) / 16 (fp32)";
+    if (c->head_dim != 64 && c->head_dim != 128) return "head_dim must be 64 or 128";
+    if (c->n_heads < 1 || c->n_kv_heads < 1 || c->n_heads % c->n_kv_heads) return "n_heads must be a multiple of n_kv_heads";
+    if ((c->n_heads * c->head_dim) % kc) return "n_heads*head_dim not a multiple of the K chunk";
+    if (c->ffn_dim <= 0 || c->ffn_dim % kc || c->ffn_dim % 8) return "ffn_dim must be a positive multiple of 32 (bf16) / 16 (fp32)";
+    if (c->vocab <= 0 || c->vocab % 16) return "vocab must be a positive multiple of 16";
+    if (c->max_batch < 1 || c->max_k_spec < 1 || c->max_k_spec > 16) return "max_batch >= 1, 1 <= max_k_spec <= 16";
+    if (c->max_batch * c->max_k_spec > kMaxRows) return "max_batch * max_k_spec must be <= 64";
+    if (c->max_seq < 2) return "max_seq < 2";
+    if (c->lora_rank < 1 || c->lora_rank > 64) return "lora_rank must be in [1, 64]";
+    if (c->buffer_rows < 1) return "buffer_rows < 1";
+    if (!(c->rms_eps > 0.f) || !(c->rope_theta > 0.f)) return "rms_eps and rope_theta must be > 0";
+    return nullptr;
+}
+
+extern "C" size_t dvi_workspace_bytes(const dvi_config *cfg) {
+    if (check_config(cfg)) return 0;
+    return layout(nullptr, *cfg, nullptr);
+}
+
+static dvi_status to_f32_vec(dvi_ctx *x, const void *src_dev, size_t n, float *dst_dev) {
+    std::vector<uint8_t> tmp(n * x->es);
+    std::vector<float> f(n);
+    HIPCHK(x, hipMemcpy(tmp.data(), src_dev, n * x->es, hipMemcpyDeviceToHost));
+    for (size_t i = 0; i < n; ++i) {
+        if (x->dt == DType::BF16) {
+            uint32_t u = (uint32_t)((uint16_t *)tmp.data())[i] << 16;
+            memcpy(&f[i], &u, 4);
+        } else {
+            f[i] = ((float *)tmp.data())[i];
+        }
+    }
+    HIPCHK(x, hipMemcpy(dst_dev, f.data(), n * 4, hipMemcpyHostToDevice));
+    return DVI_OK;
+}
+
+static dvi_status pack(dvi_ctx *x, PackSrc s, const std::vector<int32_t> &prow, int N, int K, void *dst) {
+    HIPCHK(x, hipMemcpy(x->prow, prow.data(), prow.size() * 4, hipMemcpyHostToDevice));
+    launch_pack(x->dt, s, x->prow, N, K, dst, x->stream);
+    LAUNCHCHK(x);
+    HIPCHK(x, hipStreamSynchronize(x->stream));
+    return DVI_OK;
+}
+
+static inline int32_t code(int src, int row) { return (src << 24) | row; }
+
+extern "C" dvi_status dvi_create(const dvi_config *cfg, const dvi_weights *w, void *ws, size_t ws_bytes, void *stream,
+                                 dvi_ctx **out) {
+    if (!out) return DVI_ERR_ARG;
+    *out = nullptr;
+    const char *why = check_config(cfg);
+    if (why) return DVI_ERR_ARG;
+    if (!w || !ws) return DVI_ERR_ARG;
+    if (((uintptr_t)ws) & 255) return DVI_ERR_ARG;
+    const size_t need = layout(nullptr, *cfg, nullptr);
+    if (ws_bytes < need) return DVI_ERR_CAPACITY;
+    dvi_ctx *x = new dvi_ctx();
+    x->cfg = *cfg;
+    x->dt = cfg->dtype == DVI_BF16 ? DType::BF16 : DType::F32;
+    x->es = dtype_size(x->dt);
+    x->stream = (hipStream_t)stream;
+    layout(x, *cfg, ws);
+    x->lora_A = w->lora_A;
+    x->lora_B = w->lora_B;
+    const dvi_config &c = *cfg;
+    const int d = c.d_model, F = c.ffn_dim, V = c.vocab, hd = c.head_dim, H = c.n_heads, Hkv = c.n_kv_heads;
+    dvi_status st;
+#define TRY(e)                            \
+    do {                                  \
+        st = (e);                         \
+        if (st != DVI_OK) {               \
+            *out = x;                     \
+            return st;                    \
+        }                                 \
+    } while (0)
+    // Row orders.  QKV: inside every head, packed local row 4g+2p+s (g = 0..3, p, s = 0..1) of
+    // tile t is head dim j + s*hd/2 with j = 8t + 2g + p, so an MFMA lane holds both members of
+    // two rotary pairs.  Gate/up: local row 4g+2p+s of tile t is feature 8t+2g+p of the gate
+    // (s = 0) or up (s = 1) projection, so a lane holds (gate, up) of two features.
+    std::vector<int32_t> pq(qkv_rows(c)), pgu(2 * F), pid_d(d), pid_v(V);
+    for (int i = 0; i < qkv_rows(c); ++i) {
+        const int hg = i / hd, loc = i % hd, t = loc / 16, lr = loc % 16;
+        const int g = lr / 4, p = (lr % 4) / 2, s = lr % 2;
+        const int dim = 8 * t + 2 * g + p + s * (hd / 2);
+        if (hg < H) pq[i] = code(0, hg * hd + dim);
+        else if (hg < H + Hkv) pq[i] = code(1, (hg - H) * hd + dim);
+        else pq[i] = code(2, (hg - H - Hkv) * hd + dim);
+    }
+    for (int i = 0; i < 2 * F; ++i) {
+        const int t = i / 16, lr = i % 16, g = lr / 4, p = (lr % 4) / 2, s = lr % 2;
+        pgu[i] = code(s, 8 * t + 2 * g + p);
+    }
+    for (int i = 0; i < d; ++i) pid_d[i] = code(0, i);
+    for (int i = 0; i < V; ++i) pid_v[i] = code(0, i);
+    for (int l = 0; l < c.n_layers; ++l) {
+        PackSrc s{};
+        s.src[0] = w->wq[l]; s.src[1] = w->wk[l]; s.src[2] = w->wv[l];
+        TRY(pack(x, s, pq, qkv_rows(c), d, x->L[l].wqkv));
+        s.src[0] = w->wo[l];
+        TRY(pack(x, s, pid_d, d, H * hd, x->L[l].wo));
+        s.src[0] = w->w_gate[l]; s.src[1] = w->w_up[l];
+        TRY(pack(x, s, pgu, 2 * F, d, x->L[l].wgu));
+        s.src[0] = w->w_down[l];
+        TRY(pack(x, s, pid_d, d, F, x->L[l].wd));
+        TRY(to_f32_vec(x, w->attn_norm[l], d, x->L[l].attn_norm));
+        TRY(to_f32_vec(x, w->mlp_norm[l], d, x->L[l].mlp_norm));
+    }
+    {
+        PackSrc s{};
+        s.src[0] = w->lm_head;
+        TRY(pack(x, s, pid_v, V, d, x->head));
+    }
+    TRY(to_f32_vec(x, w->final_norm, d, x->final_norm));
+    if (hipMemcpy(x->emb, w->tok_emb, (size_t)V * d * x->es, hipMemcpyDeviceToDevice) != hipSuccess) {
+        *out = x;
+        return fail(x, DVI_ERR_DEVICE, "embedding copy failed");
+    }
+    // Rotary table: entry (p, j) = (cos, sin) of p * theta^(-2j/hd), computed in double.
+    {
+        std::vector<float> rt((size_t)c.max_seq * (hd / 2) * 2);
+        for (int p = 0; p < c.max_seq; ++p)
+            for (int j = 0; j < hd / 2; ++j) {
+                const double ang = (double)p * pow((double)c.rope_theta, -2.0 * j / (double)hd);
+                rt[((size_t)p * (hd / 2) + j) * 2 + 0] = (float)cos(ang);
+                rt[((size_t)p * (hd / 2) + j) * 2 + 1] = (float)sin(ang);
+            }
+        if (hipMemcpy(x->rope, rt.data(), rt.size() * 4, hipMemcpyHostToDevice) != hipSuccess) {
+            *out = x;
+            return fail(x, DVI_ERR_DEVICE, "rope upload failed");
+        }
+    }
+    // Zero the small state, ring and optimiser moments.
+    {
+        const size_t Bk = (size_t)c.max_batch * c.max_k_spec;
+        const size_t R = c.buffer_rows, r = c.lora_rank;
+        struct Z { void *p; size_t n; } zs[] = {
+            {x->lens, (size_t)c.max_batch * 4}, {x->pending, (size_t)c.max_batch * 4}, {x->drafts, Bk * 4},
+            {x->targets, Bk * 4}, {x->io, (Bk + 2 * (size_t)c.max_batch + 4) * 4}, {x->ring_state, 16},
+            {x->ring_fresh, R}, {x->ring_r, R}, {x->mA, (size_t)V * r * 4}, {x->vA, (size_t)V * r * 4},
+            {x->mB, r * d * 4}, {x->vB, r * d * 4}};
+        for (const Z &z : zs)
+            if (hipMemset(z.p, 0, z.n) != hipSuccess) {
+                *out = x;
+                return fail(x, DVI_ERR_DEVICE, "zero-fill failed");
+            }
+        if (hipDeviceSynchronize() != hipSuccess) {
+            *out = x;
+            return fail(x, DVI_ERR_DEVICE, "zero-fill failed");
+        }
+    }
+#undef TRY
+    x->ev_ok = true;
+    for (int i = 0; i < 8; ++i)
+        if (hipEventCreate(&x->ev[i]) != hipSuccess) x->ev_ok = false;
+    x->lens_h.assign(c.max_batch, 0);
+    x->state = S_CREATED;
+    *out = x;
+    return DVI_OK;
+}
+
+extern "C" void dvi_destroy(dvi_ctx *x) {
+    if (!x) return;
+    if (x->ev_ok)
+        for (int i = 0; i < 8; ++i) (void)hipEventDestroy(x->ev[i]);
+    for (auto &e : x->pev) (void)hipEventDestroy(e);
+    delete x;
+}
+
+extern "C" const char *dvi_last_error(const dvi_ctx *x) { return x ? x->err : "null context"; }
+
+// ------------------------------------------------------------------------------------------
+// forward pieces
+// ------------------------------------------------------------------------------------------
+constexpr size_t kProbeMax = 8192;
+
+static bool probe_begin(dvi_ctx *x, int cls) {
+    if (x->probe != cls || x->pused + 2 > x->pev.size()) return false;
+    return hipEventRecord(x->pev[x->pused], x->stream) == hipSuccess;
+}
+static void probe_end(dvi_ctx *x, double bytes) {
+    if (hipEventRecord(x->pev[x->pused + 1], x->stream) == hipSuccess) {
+        x->pused += 2;
+        x->plaunch += 1;
+        x->pbytes += bytes;
+    }
+}
+
+// Algorithmic bytes of one GEMM launch: the weight matrix once, activations in, results out.
+static double gemm_bytes(const dvi_ctx *x, Epi e, int M, int N, int K) {
+    const double es = (double)x->es;
+    double b = (double)N * K * es + (double)M * K * es;
+    const dvi_config &c = x->cfg;
+    switch (e) {
+        case EPI_RESID: b += 2.0 * M * N * 4; break;                               // h read + written
+        case EPI_QKV: b += (double)M * c.n_heads * c.head_dim * 4 + 2.0 * M * c.n_kv_heads * c.head_dim * es; break;
+        case EPI_SWIGLU: b += (double)M * (N / 2) * es; break;
+        case EPI_LOGITS: b += (double)M * N * 4; break;
+    }
+    return b;
+}
+
+static void gemm(dvi_ctx *x, Epi e, int cls, const void *W, const void *X, int M, int N, int K, GemmArgs a) {
+    a.W = W;
+    a.X = X;
+    a.M = M;
+    a.N = N;
+    a.K = K;
+    const bool pr = probe_begin(x, cls);
+    launch_gemm(x->dt, e, a, x->stream);
+    if (pr) probe_end(x, gemm_bytes(x, e, M, N, K));
+}
+
+// Layers [l0, l1) on M = B*c rows of h; row b*c+i sits at position lens[b] + pos_off + i.
+static dvi_status run_layers(dvi_ctx *x, int l0, int l1, int B, int c, int pos_off, float *h) {
+    const dvi_config &cf = x->cfg;
+    const int d = cf.d_model, F = cf.ffn_dim, H = cf.n_heads, Hkv = cf.n_kv_heads, hd = cf.head_dim;
+    const int M = B * c;
+    int pmax = 0;
+    for (int b = 0; b < B; ++b) {
+        const int p = x->lens_h[b] + pos_off + c - 1;
+        if (p > pmax) pmax = p;
+    }
+    for (int l = l0; l < l1; ++l) {
+        const LayerW &Lw = x->L[l];
+        launch_rmsnorm(x->dt, h, Lw.attn_norm, M, d, cf.rms_eps, x->xn, x->stream);
+        GemmArgs a{};
+        a.c = c;
+        a.pos_off = pos_off;
+        a.lens = x->lens;
+        a.Q = x->q;
+        a.Kc = Lw.Kc;
+        a.Vc = Lw.Vc;
+        a.n_heads = H;
+        a.n_kv = Hkv;
+        a.hd = hd;
+        a.s_max = cf.max_seq;
+        a.rope = x->rope;
+        gemm(x, EPI_QKV, DVI_PROBE_QKV, Lw.wqkv, x->xn, M, qkv_rows(cf), d, a);
+        AttnArgs at{};
+        at.Q = x->q;
+        at.Kc = Lw.Kc;
+        at.Vc = Lw.Vc;
+        at.lens = x->lens;
+        at.B = B;
+        at.c = c;
+        at.pos_off = pos_off;
+        at.n_heads = H;
+        at.n_kv = Hkv;
+        at.hd = hd;
+        at.s_max = cf.max_seq;
+        at.n_chunks = pmax / kChunk + 1;
+        at.chunk_stride = x->chunk_stride;
+        at.scale = 1.0f / sqrtf((float)hd);
+        at.part_o = x->att_po;
+        at.part_ml = x->att_pml;
+        at.O = x->attn_o;
+        const bool pa = probe_begin(x, DVI_PROBE_ATTENTION);
+        launch_attention(x->dt, at, x->stream);
+        if (pa) {
+            // keys and values of positions 0..p read once per (sequence, kv head); q in, o out
+            double kv = 0.0;
+            for (int b = 0; b < B; ++b) kv += (double)(x->lens_h[b] + pos_off + c) * Hkv * hd * 2.0 * x->es;
+            probe_end(x, kv + (double)M * H * hd * (4.0 + x->es));
+        }
+        GemmArgs r{};
+        r.H = h;
+        gemm(x, EPI_RESID, DVI_PROBE_ATTN_OUT, Lw.wo, x->attn_o, M, d, H * hd, r);
+        launch_rmsnorm(x->dt, h, Lw.mlp_norm, M, d, cf.rms_eps, x->xn, x->stream);
+        GemmArgs g{};
+        g.A = x->act;
+        gemm(x, EPI_SWIGLU, DVI_PROBE_GATE_UP, Lw.wgu, x->xn, M, 2 * F, d, g);
+        gemm(x, EPI_RESID, DVI_PROBE_DOWN, Lw.wd, x->act, M, d, F, r);
+    }
+    LAUNCHCHK(x);
+    return DVI_OK;
+}
+
+// io block: tokens [max_batch*max_k_spec] | n [max_batch] | m [max_batch] | flags [4]
+static int io_n(const dvi_ctx *x) { return x->cfg.max_batch * x->cfg.max_k_spec; }
+static int io_m(const dvi_ctx *x) { return io_n(x) + x->cfg.max_batch; }
+static int io_flags(const dvi_ctx *x) { return io_m(x) + x->cfg.max_batch; }
+static int io_words(const dvi_ctx *x) { return io_flags(x) + 4; }
+static int32_t *flags_ptr(dvi_ctx *x) { return x->io + io_flags(x); }
+
+// Vocabulary head on M normalised rows in x->xn: logits -> Z, argmax -> out (stride).
+static void head(dvi_ctx *x, int M, float *Z, bool lora, int32_t *out, int out_stride, const int32_t *forced) {
+    const dvi_config &cf = x->cfg;
+    GemmArgs a{};
+    a.Z = Z;
+    a.part_val = x->part_val;
+    a.part_idx = x->part_idx;
+    if (lora) {
+        launch_lora_u(x->dt, x->xn, x->lora_B, M, cf.d_model, cf.lora_rank, x->lora_u, x->stream);
+        a.lora_A = x->lora_A;
+        a.lora_u = x->lora_u;
+        a.r = cf.lora_rank;
+        a.gamma = cf.lora_gamma;
+    }
+    gemm(x, EPI_LOGITS, DVI_PROBE_HEAD, x->head, x->xn, M, cf.vocab, cf.d_model, a);
+    launch_argmax(x->part_val, x->part_idx, M, cf.vocab / 16, out, out_stride, forced, flags_ptr(x), x->stream);
+}
+
+static void ev_begin(dvi_ctx *x, int phase) {
+    if (x->ev_ok) (void)hipEventRecord(x->ev[2 * phase], x->stream);
+}
+static void ev_end(dvi_ctx *x, int phase) {
+    if (x->ev_ok) {
+        (void)hipEventRecord(x->ev[2 * phase + 1], x->stream);
+        x->ev_pending[phase] = 1;
+    }
+}
+
+// ------------------------------------------------------------------------------------------
+// C ABI: decode step
+// ------------------------------------------------------------------------------------------
+extern "C" dvi_status dvi_prefill(dvi_ctx *x, int32_t batch, const int32_t *ids, const int32_t *lens, int32_t stride,
+                                  int32_t *first_tok) {
+    if (!x) return DVI_ERR_ARG;
+    if (x->device_error) return fail(x, DVI_ERR_DEVICE, "context has a sticky device error");
+    if (x->state == S_DRAFTED || x->state == S_VERIFIED) return fail(x, DVI_ERR_STATE, "prefill during a step");
+    const dvi_config &cf = x->cfg;
+    if (!ids || !lens || !first_tok) return fail(x, DVI_ERR_ARG, "null argument");
+    if (batch < 1) return fail(x, DVI_ERR_ARG, "batch < 1");
+    if (batch > cf.max_batch) return fail(x, DVI_ERR_CAPACITY, "batch %d > max_batch %d", batch, cf.max_batch);
+    const int P = lens[0];
+    for (int b = 0; b < batch; ++b)
+        if (lens[b] != P) return fail(x, DVI_ERR_ARG, "prompt lengths must be equal");
+    if (P < 1 || P > stride) return fail(x, DVI_ERR_ARG, "prompt length must be in [1, stride]");
+    if (P + 1 > cf.max_seq) return fail(x, DVI_ERR_CAPACITY, "prompt length %d leaves no room in max_seq %d", P, cf.max_seq);
+    std::vector<int32_t> packed((size_t)batch * P);
+    for (int b = 0; b < batch; ++b)
+        for (int i = 0; i < P; ++i) {
+            const int32_t t = ids[(size_t)b * stride + i];
+            if (t < 0 || t >= cf.vocab) return fail(x, DVI_ERR_ARG, "token id %d out of range", t);
+            packed[(size_t)b * P + i] = t;
+        }
+    const int d = cf.d_model;
+    HIPCHK(x, hipMemcpyAsync(x->ids, packed.data(), packed.size() * 4, hipMemcpyHostToDevice, x->stream));
+    HIPCHK(x, hipMemsetAsync(x->lens, 0, cf.max_batch * 4, x->stream));
+    HIPCHK(x, hipMemsetAsync(flags_ptr(x), 0, 16, x->stream));
+    x->B = batch;
+    for (int b = 0; b < cf.max_batch; ++b) x->lens_h[b] = 0;
+    const int c = (kMaxRows / batch) < 1 ? 1 : kMaxRows / batch;
+    for (int s0 = 0; s0 < P; s0 += c) {
+        const int cc = (P - s0) < c ? P - s0 : c;
+        launch_embed(x->dt, x->emb, x->ids + s0, P, batch, cc, d, x->h, x->stream);
+        dvi_status st = run_layers(x, 0, cf.n_layers, batch, cc, s0, x->h);
+        if (st != DVI_OK) return st;
+        if (s0 + cc == P) {
+            launch_copy_rows(x->h + (size_t)(cc - 1) * d, cc, x->hk, 1, batch, d, x->stream);
+            launch_rmsnorm(x->dt, x->hk, x->final_norm, batch, d, cf.rms_eps, x->xn, x->stream);
+            head(x, batch, x->vlogits, false, x->pending, 1, nullptr);
+        }
+    }
+    std::vector<int32_t> lh(cf.max_batch, 0);
+    for (int b = 0; b < batch; ++b) lh[b] = P;
+    HIPCHK(x, hipMemcpyAsync(x->lens, lh.data(), cf.max_batch * 4, hipMemcpyHostToDevice, x->stream));
+    int32_t fl[4];
+    HIPCHK(x, hipMemcpyAsync(first_tok, x->pending, batch * 4, hipMemcpyDeviceToHost, x->stream));
+    HIPCHK(x, hipMemcpyAsync(fl, flags_ptr(x), 16, hipMemcpyDeviceToHost, x->stream));
+    HIPCHK(x, hipStreamSynchronize(x->stream));
+    LAUNCHCHK(x);
+    for (int b = 0; b < batch; ++b) x->lens_h[b] = P;
+    x->k_spec = 1;  // dvi_read_logits now returns the prefill's head logits, one row per sequence
+    x->state = S_READY;
+    if (fl[0]) return fail(x, DVI_ERR_NUMERIC, "non-finite logits in prefill");
+    return DVI_OK;
+}
+
+extern "C" dvi_status dvi_draft(dvi_ctx *x, int32_t k_spec, const int32_t *forced, int32_t *drafts_out) {
+    if (!x) return DVI_ERR_ARG;
+    if (x->device_error) return fail(x, DVI_ERR_DEVICE, "context has a sticky device error");
+    if (x->state != S_READY) return fail(x, DVI_ERR_STATE, "draft needs state READY");
+    const dvi_config &cf = x->cfg;
+    if (k_spec < 1) return fail(x, DVI_ERR_ARG, "k_spec < 1");
+    if (k_spec > cf.max_k_spec) return fail(x, DVI_ERR_CAPACITY, "k_spec %d > max_k_spec %d", k_spec, cf.max_k_spec);
+    for (int b = 0; b < x->B; ++b)
+        if (x->lens_h[b] + k_spec > cf.max_seq)
+            return fail(x, DVI_ERR_CAPACITY, "sequence %d: length %d + k_spec %d > max_seq %d", b, x->lens_h[b], k_spec,
+                        cf.max_seq);
+    const int B = x->B, d = cf.d_model;
+    if (forced) {
+        for (int i = 0; i < B * k_spec; ++i)
+            if (forced[i] < 0 || forced[i] >= cf.vocab) return fail(x, DVI_ERR_ARG, "forced draft id out of range");
+        HIPCHK(x, hipMemcpyAsync(x->forced, forced, (size_t)B * k_spec * 4, hipMemcpyHostToDevice, x->stream));
+    }
+    ev_begin(x, 0);
+    HIPCHK(x, hipMemsetAsync(flags_ptr(x), 0, 16, x->stream));
+    x->ar_mode = (k_spec == 1 && !forced) ? 1 : 0;
+    for (int j = 0; j < k_spec; ++j) {
+        const int32_t *tok = j == 0 ? x->pending : x->drafts + (j - 1);
+        launch_embed(x->dt, x->emb, tok, j == 0 ? 1 : k_spec, B, 1, d, x->h, x->stream);
+        dvi_status st = run_layers(x, 0, cf.split_k, B, 1, j, x->h);
+        if (st != DVI_OK) return st;
+        launch_scatter_rows(x->h, x->hk, B, d, 4, k_spec, j, x->stream);
+        launch_rmsnorm(x->dt, x->h, x->final_norm, B, d, cf.rms_eps, x->xn, x->stream);
+        launch_scatter_rows(x->xn, x->hk_hat, B, d, (int)x->es, k_spec, j, x->stream);
+        if (!x->ar_mode) head(x, B, x->dlogits, true, x->drafts + j, k_spec, forced ? x->forced + j : nullptr);
+    }
+    if (x->ar_mode) HIPCHK(x, hipMemsetAsync(x->drafts, 0xff, (size_t)B * 4, x->stream));
+    ev_end(x, 0);
+    LAUNCHCHK(x);
+    x->k_spec = k_spec;
+    if (drafts_out) {
+        HIPCHK(x, hipMemcpyAsync(drafts_out, x->drafts, (size_t)B * k_spec * 4, hipMemcpyDeviceToHost, x->stream));
+        HIPCHK(x, hipStreamSynchronize(x->stream));
+    }
+    x->state = S_DRAFTED;
+    return DVI_OK;
+}
+
+extern "C" dvi_status dvi_verify(dvi_ctx *x, int32_t *targets_out, int32_t *accept_out) {
+    if (!x) return DVI_ERR_ARG;
+    if (x->device_error) return fail(x, DVI_ERR_DEVICE, "context has a sticky device error");
+    if (x->state != S_DRAFTED) return fail(x, DVI_ERR_STATE, "verify needs state DRAFTED");
+    const dvi_config &cf = x->cfg;
+    const int B = x->B, k = x->k_spec, M = B * k, d = cf.d_model;
+    ev_begin(x, 1);
+    dvi_status st = run_layers(x, cf.split_k, cf.n_layers, B, k, 0, x->hk);
+    if (st != DVI_OK) return st;
+    launch_rmsnorm(x->dt, x->hk, x->final_norm, M, d, cf.rms_eps, x->xn, x->stream);
+    head(x, M, x->vlogits, false, x->targets, 1, nullptr);
+    ev_end(x, 1);
+    LAUNCHCHK(x);
+    if (targets_out || accept_out) {
+        std::vector<int32_t> tg((size_t)M), dr((size_t)M);
+        HIPCHK(x, hipMemcpyAsync(tg.data(), x->targets, (size_t)M * 4, hipMemcpyDeviceToHost, x->stream));
+        HIPCHK(x, hipMemcpyAsync(dr.data(), x->drafts, (size_t)(x->ar_mode ? B : M) * 4, hipMemcpyDeviceToHost,
+                                 x->stream));
+        HIPCHK(x, hipStreamSynchronize(x->stream));
+        if (targets_out) memcpy(targets_out, tg.data(), (size_t)M * 4);
+        if (accept_out)
+            for (int b = 0; b < B; ++b) {
+                int m = 0;
+                if (!x->ar_mode)
+                    while (m < k && dr[(size_t)b * k + m] == tg[(size_t)b * k + m]) ++m;
+                accept_out[b] = m;
+            }
+    }
+    x->state = S_VERIFIED;
+    return DVI_OK;
+}
+
+extern "C" dvi_status dvi_commit(dvi_ctx *x, const int32_t *max_new, const int32_t *forced_commit, int32_t *tokens_out,
+                                 int32_t *n_out, int32_t *accept_out) {
+    if (!x) return DVI_ERR_ARG;
+    if (x->device_error) return fail(x, DVI_ERR_DEVICE, "context has a sticky device error");
+    if (x->state != S_VERIFIED) return fail(x, DVI_ERR_STATE, "commit needs state VERIFIED");
+    if (!tokens_out || !n_out) return fail(x, DVI_ERR_ARG, "null output");
+    const dvi_config &cf = x->cfg;
+    const int B = x->B, k = x->k_spec;
+    if (forced_commit) {
+        for (int i = 0; i < B * k; ++i)
+            if (forced_commit[i] < 0 || forced_commit[i] >= cf.vocab)
+                return fail(x, DVI_ERR_ARG, "forced commit id out of range");
+        HIPCHK(x, hipMemcpyAsync(x->targets, forced_commit, (size_t)B * k * 4, hipMemcpyHostToDevice, x->stream));
+    }
+    if (max_new) {
+        for (int b = 0; b < B; ++b)
+            if (max_new[b] < 0) return fail(x, DVI_ERR_ARG, "max_new < 0");
+        HIPCHK(x, hipMemcpyAsync(x->max_new, max_new, (size_t)B * 4, hipMemcpyHostToDevice, x->stream));
+    }
+    ev_begin(x, 2);
+    CommitArgs a{};
+    a.B = B;
+    a.k_spec = k;
+    a.drafts = x->drafts;
+    a.targets = x->targets;
+    a.max_new = max_new ? x->max_new : nullptr;
+    a.lens = x->lens;
+    a.pending = x->pending;
+    a.tokens_out = x->io;
+    a.n_out = x->io + io_n(x);
+    a.m_out = x->io + io_m(x);
+    a.flags = flags_ptr(x);
+    a.ring_state = x->ring_state;
+    a.ring_rows = x->ar_mode ? 0 : cf.buffer_rows;
+    a.copy_list = x->copy_list;
+    a.ring_a = x->ring_a;
+    a.ring_i = x->ring_i;
+    a.ring_prev = x->ring_prev;
+    a.ring_r = x->ring_r;
+    a.ring_fresh = x->ring_fresh;
+    if (x->ar_mode) {
+        // plain autoregressive step: nothing was drafted; commit y*_1 only
+        HIPCHK(x, hipMemsetAsync(x->drafts, 0xff, (size_t)B * 4, x->stream));
+    }
+    launch_commit(a, x->stream);
+    if (!x->ar_mode)
+        launch_ring_copy(x->copy_list, B * k, x->hk_hat, cf.d_model, (int)x->es, x->vlogits, cf.vocab, x->ring_h,
+                         x->ring_logits, x->stream);
+    ev_end(x, 2);
+    LAUNCHCHK(x);
+    std::vector<int32_t> io((size_t)io_words(x));
+    HIPCHK(x, hipMemcpyAsync(io.data(), x->io, io.size() * 4, hipMemcpyDeviceToHost, x->stream));
+    HIPCHK(x, hipStreamSynchronize(x->stream));
+    // Non-finite logits: the commit kernel committed nothing; the caller aborts the step.
+    if (io[io_flags(x)]) return fail(x, DVI_ERR_NUMERIC, "non-finite logits in the draft or verify head");
+    memcpy(tokens_out, io.data(), (size_t)B * k * 4);
+    memcpy(n_out, io.data() + io_n(x), (size_t)B * 4);
+    if (accept_out) memcpy(accept_out, io.data() + io_m(x), (size_t)B * 4);
+    for (int b = 0; b < B; ++b) {
+        x->lens_h[b] += io[io_n(x) + b];
+        const int m = io[io_m(x) + b];
+        const bool logged = !x->ar_mode && (!max_new || max_new[b] > 0);
+        if (logged) {
+            x->ring_valid_h += (m + 1 < k ? m + 1 : k);
+            if (x->ring_valid_h > cf.buffer_rows) x->ring_valid_h = cf.buffer_rows;
+        }
+    }
+    x->state = S_READY;
+    return DVI_OK;
+}
+
+extern "C" dvi_status dvi_abort_step(dvi_ctx *x) {
+    if (!x) return DVI_ERR_ARG;
+    if (x->state != S_DRAFTED && x->state != S_VERIFIED) return fail(x, DVI_ERR_STATE, "no step in progress");
+    HIPCHK(x, hipMemsetAsync(flags_ptr(x), 0, 16, x->stream));
+    x->state = S_READY;
+    return DVI_OK;
+}
+
+// ------------------------------------------------------------------------------------------
+// C ABI: drafter update
+// ------------------------------------------------------------------------------------------
+__global__ void clear_i8_kernel(int8_t *p, int n) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = 0;
+}
+
+extern "C" dvi_status dvi_update_drafter(dvi_ctx *x, const dvi_update_args *ua, dvi_update_stats *stats) {
+    if (!x || !ua) return DVI_ERR_ARG;
+    if (x->device_error) return fail(x, DVI_ERR_DEVICE, "context has a sticky device error");
+    if (x->state != S_READY) return fail(x, DVI_ERR_STATE, "update needs state READY");
+    if (!(ua->tau > 0.f)) return fail(x, DVI_ERR_ARG, "tau must be > 0");
+    if (ua->lr != 0.f && ua->opt_step < 1) return fail(x, DVI_ERR_ARG, "opt_step must be >= 1");
+    const dvi_config &cf = x->cfg;
+    const int n = x->ring_valid_h;
+    if (stats) memset(stats, 0, sizeof(*stats));
+    if (n == 0) return DVI_OK;
+    ev_begin(x, 3);
+    UpdateArgs u{};
+    u.W = x->head;
+    u.Hh = x->ring_h;
+    u.logits = x->ring_logits;
+    u.a = x->ring_a;
+    u.r = x->ring_r;
+    u.fresh = x->ring_fresh;
+    u.n = n;
+    u.V = cf.vocab;
+    u.d = cf.d_model;
+    u.rank = cf.lora_rank;
+    u.gamma = cf.lora_gamma;
+    u.tau = ua->tau;
+    u.baseline = ua->baseline;
+    u.c_kl = ua->c_kl;
+    u.c_ce = ua->c_ce;
+    u.c_pg = ua->c_pg;
+    u.c_ent = ua->c_ent;
+    u.A = x->lora_A;
+    u.Bm = x->lora_B;
+    u.u = x->upd_u;
+    u.Z = x->upd_Z;
+    u.part_val = x->part_val;
+    u.part_idx = x->part_idx;
+    u.row_stats = x->upd_stats;
+    u.dA = x->upd_dA;
+    u.du = x->upd_du;
+    u.dB = x->upd_dB;
+    u.loss_out = x->upd_loss;
+    launch_update_forward(x->dt, u, x->stream);
+    launch_update_backward(x->dt, u, x->stream);
+    const size_t nA = (size_t)cf.vocab * cf.lora_rank, nB = (size_t)cf.lora_rank * cf.d_model;
+    if (ua->grad_A_out)
+        HIPCHK(x, hipMemcpyAsync(ua->grad_A_out, x->upd_dA, nA * 4, hipMemcpyDeviceToDevice, x->stream));
+    if (ua->grad_B_out)
+        HIPCHK(x, hipMemcpyAsync(ua->grad_B_out, x->upd_dB, nB * 4, hipMemcpyDeviceToDevice, x->stream));
+    if (ua->lr != 0.f) {
+        launch_adam(x->lora_A, x->upd_dA, x->mA, x->vA, (int)nA, ua->lr, ua->beta1, ua->beta2, ua->eps, ua->opt_step,
+                    x->stream);
+        launch_adam(x->lora_B, x->upd_dB, x->mB, x->vB, (int)nB, ua->lr, ua->beta1, ua->beta2, ua->eps, ua->opt_step,
+                    x->stream);
+    }
+    clear_i8_kernel<<<(cf.buffer_rows + 255) / 256, 256, 0, x->stream>>>(x->ring_fresh, cf.buffer_rows);
+    ev_end(x, 3);
+    LAUNCHCHK(x);
+    float lo[16];
+    HIPCHK(x, hipMemcpyAsync(lo, x->upd_loss, 16 * 4, hipMemcpyDeviceToHost, x->stream));
+    HIPCHK(x, hipStreamSynchronize(x->stream));
+    if (stats) {
+        stats->loss = lo[0];
+        stats->kl = lo[1];
+        stats->ce = lo[2];
+        stats->pg = lo[3];
+        stats->entropy = lo[4];
+        stats->rows = (int32_t)lo[5];
+        stats->accepted = (int32_t)lo[6];
+        stats->fresh = (int32_t)lo[7];
+        stats->fresh_accepted = (int32_t)lo[8];
+    }
+    return DVI_OK;
+}
+
+// ------------------------------------------------------------------------------------------
+// C ABI: inspection and test hooks
+// ------------------------------------------------------------------------------------------
+extern "C" dvi_status dvi_read_kv(dvi_ctx *x, int32_t layer, int32_t seq, int32_t pos0, int32_t npos, void *k, void *v) {
+    if (!x || !k || !v) return DVI_ERR_ARG;
+    const dvi_config &cf = x->cfg;
+    if (layer < 0 || layer >= cf.n_layers || seq < 0 || seq >= cf.max_batch || pos0 < 0 || npos < 0 ||
+        pos0 + npos > cf.max_seq)
+        return fail(x, DVI_ERR_ARG, "read_kv range");
+    const size_t row = (size_t)cf.head_dim * x->es;
+    for (int h = 0; h < cf.n_kv_heads; ++h) {
+        const size_t off = (((size_t)seq * cf.n_kv_heads + h) * cf.max_seq + pos0) * row;
+        HIPCHK(x, hipMemcpyAsync((uint8_t *)k + (size_t)h * npos * row, (uint8_t *)x->L[layer].Kc + off, npos * row,
+                                 hipMemcpyDeviceToHost, x->stream));
+        HIPCHK(x, hipMemcpyAsync((uint8_t *)v + (size_t)h * npos * row, (uint8_t *)x->L[layer].Vc + off, npos * row,
+                                 hipMemcpyDeviceToHost, x->stream));
+    }
+    HIPCHK(x, hipStreamSynchronize(x->stream));
+    return DVI_OK;
+}
+
+extern "C" dvi_status dvi_read_logits(dvi_ctx *x, float *out) {
+    if (!x || !out) return DVI_ERR_ARG;
+    if (x->state != S_VERIFIED && x->state != S_READY) return fail(x, DVI_ERR_STATE, "no verify logits");
+    HIPCHK(x, hipMemcpyAsync(out, x->vlogits, (size_t)x->B * x->k_spec * x->cfg.vocab * 4, hipMemcpyDeviceToHost,
+                             x->stream));
+    HIPCHK(x, hipStreamSynchronize(x->stream));
+    return DVI_OK;
+}
+
+extern "C" dvi_status dvi_read_draft_logits(dvi_ctx *x, float *out) {
+    if (!x || !out) return DVI_ERR_ARG;
+    HIPCHK(x, hipMemcpyAsync(out, x->dlogits, (size_t)x->B * x->cfg.vocab * 4, hipMemcpyDeviceToHost, x->stream));
+    HIPCHK(x, hipStreamSynchronize(x->stream));
+    return DVI_OK;
+}
+
+extern "C" dvi_status dvi_read_lengths(dvi_ctx *x, int32_t *len) {
+    if (!x || !len) return DVI_ERR_ARG;
+    HIPCHK(x, hipMemcpyAsync(len, x->lens, (size_t)x->B * 4, hipMemcpyDeviceToHost, x->stream));
+    HIPCHK(x, hipStreamSynchronize(x->stream));
+    return DVI_OK;
+}
+
+extern "C" dvi_status dvi_buffer_info(dvi_ctx *x, int32_t *valid, int32_t *next) {
+    if (!x) return DVI_ERR_ARG;
+    int32_t rs[4];
+    HIPCHK(x, hipMemcpyAsync(rs, x->ring_state, 16, hipMemcpyDeviceToHost, x->stream));
+    HIPCHK(x, hipStreamSynchronize(x->stream));
+    if (valid) *valid = rs[1];
+    if (next) *next = rs[0];
+    return DVI_OK;
+}
+
+extern "C" dvi_status dvi_read_buffer(dvi_ctx *x, int32_t row0, int32_t nrows, float *h, int32_t *a, float *logits,
+                                      int8_t *r, int8_t *fresh, int32_t *i, int32_t *prev) {
+    if (!x) return DVI_ERR_ARG;
+    const dvi_config &cf = x->cfg;
+    if (row0 < 0 || nrows < 0 || row0 + nrows > cf.buffer_rows) return fail(x, DVI_ERR_ARG, "buffer range");
+    const size_t d = cf.d_model, V = cf.vocab;
+    if (h) {
+        std::vector<uint8_t> tmp((size_t)nrows * d * x->es);
+        HIPCHK(x, hipMemcpyAsync(tmp.data(), (uint8_t *)x->ring_h + (size_t)row0 * d * x->es, tmp.size(),
+                                 hipMemcpyDeviceToHost, x->stream));
+        HIPCHK(x, hipStreamSynchronize(x->stream));
+        for (size_t e = 0; e < (size_t)nrows * d; ++e) {
+            if (x->dt == DType::BF16) {
+                uint32_t u = (uint32_t)((uint16_t *)tmp.data())[e] << 16;
+                memcpy(&h[e], &u, 4);
+            } else {
+                h[e] = ((float *)tmp.data())[e];
+            }
+        }
+    }
+    if (a) HIPCHK(x, hipMemcpyAsync(a, x->ring_a + row0, nrows * 4, hipMemcpyDeviceToHost, x->stream));
+    if (i) HIPCHK(x, hipMemcpyAsync(i, x->ring_i + row0, nrows * 4, hipMemcpyDeviceToHost, x->stream));
+    if (prev) HIPCHK(x, hipMemcpyAsync(prev, x->ring_prev + row0, nrows * 4, hipMemcpyDeviceToHost, x->stream));
+    if (r) HIPCHK(x, hipMemcpyAsync(r, x->ring_r + row0, nrows, hipMemcpyDeviceToHost, x->stream));
+    if (fresh) HIPCHK(x, hipMemcpyAsync(fresh, x->ring_fresh + row0, nrows, hipMemcpyDeviceToHost, x->stream));
+    if (logits)
+        HIPCHK(x, hipMemcpyAsync(logits, x->ring_logits + (size_t)row0 * V, (size_t)nrows * V * 4,
+                                 hipMemcpyDeviceToHost, x->stream));
+    HIPCHK(x, hipStreamSynchronize(x->stream));
+    return DVI_OK;
+}
+
+extern "C" dvi_status dvi_write_buffer(dvi_ctx *x, int32_t nrows, const float *h, const int32_t *a,
+                                       const float *logits, const int8_t *r, const int8_t *fresh) {
+    if (!x || !h || !a || !logits || !r || !fresh) return DVI_ERR_ARG;
+    if (x->state == S_DRAFTED || x->state == S_VERIFIED) return fail(x, DVI_ERR_STATE, "write_buffer during a step");
+    const dvi_config &cf = x->cfg;
+    if (nrows < 1 || nrows > cf.buffer_rows) return fail(x, DVI_ERR_CAPACITY, "nrows out of range");
+    const size_t d = cf.d_model, V = cf.vocab;
+    for (int e = 0; e < nrows; ++e)
+        if (a[e] < 0 || a[e] >= cf.vocab) return fail(x, DVI_ERR_ARG, "action id out of range");
+    std::vector<uint8_t> tmp((size_t)nrows * d * x->es);
+    for (size_t e = 0; e < (size_t)nrows * d; ++e) {
+        if (x->dt == DType::BF16) {
+            uint32_t u;
+            memcpy(&u, &h[e], 4);
+            if ((u & 0x7fffffffu) > 0x7f800000u) u = (u >> 16) | 0x40;
+            else u = (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+            ((uint16_t *)tmp.data())[e] = (uint16_t)u;
+        } else {
+            ((float *)tmp.data())[e] = h[e];
+        }
+    }
+    std::vector<int32_t> zi(nrows, 0), neg(nrows, -1);
+    HIPCHK(x, hipMemcpy(x->ring_h, tmp.data(), tmp.size(), hipMemcpyHostToDevice));
+    HIPCHK(x, hipMemcpy(x->ring_logits, logits, (size_t)nrows * V * 4, hipMemcpyHostToDevice));
+    HIPCHK(x, hipMemcpy(x->ring_a, a, nrows * 4, hipMemcpyHostToDevice));
+    HIPCHK(x, hipMemcpy(x->ring_i, zi.data(), nrows * 4, hipMemcpyHostToDevice));
+    HIPCHK(x, hipMemcpy(x->ring_prev, neg.data(), nrows * 4, hipMemcpyHostToDevice));
+    HIPCHK(x, hipMemcpy(x->ring_r, r, nrows, hipMemcpyHostToDevice));
+    HIPCHK(x, hipMemcpy(x->ring_fresh, fresh, nrows, hipMemcpyHostToDevice));
+    int32_t rs[4] = {nrows % cf.buffer_rows, nrows, 0, 0};
+    HIPCHK(x, hipMemcpy(x->ring_state, rs, 16, hipMemcpyHostToDevice));
+    x->ring_valid_h = nrows;
+    return DVI_OK;
+}
+
+extern "C" dvi_status dvi_probe_kernel(dvi_ctx *x, int32_t which) {
+    if (!x) return DVI_ERR_ARG;
+    if (which < DVI_PROBE_OFF || which > DVI_PROBE_ATTENTION) return fail(x, DVI_ERR_ARG, "unknown probe %d", which);
+    if (which != DVI_PROBE_OFF && x->pev.empty()) {
+        x->pev.resize(2 * kProbeMax);
+        for (auto &e : x->pev) HIPCHK(x, hipEventCreate(&e));
+    }
+    HIPCHK(x, hipStreamSynchronize(x->stream));
+    x->probe = which;
+    x->pused = 0;
+    x->plaunch = 0;
+    x->pbytes = 0.0;
+    return DVI_OK;
+}
+
+extern "C" dvi_status dvi_probe_read(dvi_ctx *x, double *total_ms, int64_t *launches, double *bytes) {
+    if (!x) return DVI_ERR_ARG;
+    HIPCHK(x, hipStreamSynchronize(x->stream));
+    double t = 0.0;
+    for (size_t i = 0; i + 1 < x->pused; i += 2) {
+        float ms = 0.f;
+        HIPCHK(x, hipEventElapsedTime(&ms, x->pev[i], x->pev[i + 1]));
+        t += ms;
+    }
+    if (total_ms) *total_ms = t;
+    if (launches) *launches = x->plaunch;
+    if (bytes) *bytes = x->pbytes;
+    return DVI_OK;
+}
+
+extern "C" dvi_status dvi_get_timings(dvi_ctx *x, double *md, double *mv, double *mc, double *mu) {
+    if (!x) return DVI_ERR_ARG;
+    double *outs[4] = {md, mv, mc, mu};
+    for (int p = 0; p < 4; ++p) {
+        if (x->ev_ok && x->ev_pending[p]) {
+            float ms = 0.f;
+            HIPCHK(x, hipEventSynchronize(x->ev[2 * p + 1]));
+            HIPCHK(x, hipEventElapsedTime(&ms, x->ev[2 * p], x->ev[2 * p + 1]));
+            x->ms[p] = ms;
+            x->ev_pending[p] = 0;
+        }
+        if (outs[p]) *outs[p] = x->ms[p];
+    }
+    return DVI_OK;
+}

@@ -1,0 +1,148 @@
+// Internal interface between the engine (engine.hip) and the gfx950 kernels (kernels.hip).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace dvi {
+
+// Storage type of weights, activations fed to MFMA, and the KV cache.
+enum class DType { F32 = 0, BF16 = 1 };
+
+inline size_t dtype_size(DType t) { return t == DType::BF16 ? 2 : 4; }
+
+// Packed weight layout ("fragment-major"): a matrix W[N][K] is cut into tiles of 16 rows x KC
+// columns (KC = 32 for bf16, 16 for fp32), every tile 1 KiB.  Tile (nt, kt) sits at byte
+// offset (nt * (K/KC) + kt) * 1024; inside it lane l (0..63) owns 16 contiguous bytes at 16*l:
+// rows nt*16 + (l % 16), columns kt*KC + (l / 16) * EPL + [0, EPL) with EPL = KC / 4.  A wave
+// streaming one 16-row band along K therefore reads consecutive 1 KiB blocks, and each lane's
+// 16 bytes are directly its MFMA A-operand fragment.
+inline int pack_kc(DType t) { return t == DType::BF16 ? 32 : 16; }
+
+// Rows of a packed matrix may be permuted (see the epilogues): prow[i] = src * 2^24 + row
+// means packed row i is row `row` of source matrix `src` (up to three sources).
+struct PackSrc {
+    const void *src[3];
+};
+void launch_pack(DType t, PackSrc srcs, const int32_t *prow_dev, int N, int K, void *dst, hipStream_t s);
+
+enum Epi : int {
+    EPI_RESID = 0,   // H[m][n] += y                          (attention out, MLP down)
+    EPI_QKV = 1,     // rotary embed q,k; q -> Q[m]; k,v -> KV cache at the token's position
+    EPI_SWIGLU = 2,  // rows interleaved (gate f, up f): A[m][f] = silu(gate) * up
+    EPI_LOGITS = 3,  // Z[m][n] = y (+ gamma * A_s[n] . u[m]); per-tile argmax partials
+};
+
+struct GemmArgs {
+    const void *W;      // packed [N][K]
+    const void *X;      // activations [M][K] (dtype of W), row stride K
+    int M, N, K;
+    // token -> (sequence, block offset): m = b * c + i, position = lens[b] + pos_off + i
+    int c, pos_off;
+    const int32_t *lens;
+    // EPI_RESID
+    float *H;           // [M][N]
+    // EPI_QKV
+    float *Q;           // [M][n_heads * hd] fp32
+    void *Kc, *Vc;      // this layer's caches [max_batch][n_kv][s_max][hd]
+    int n_heads, n_kv, hd, s_max;
+    const float2 *rope; // [s_max][hd/2] (cos, sin)
+    // EPI_SWIGLU
+    void *A;            // [M][N/2] activations out (dtype)
+    // EPI_LOGITS
+    float *Z;           // [M][N] logits
+    const float *lora_A;// [N][r] or nullptr
+    const float *lora_u;// [M][r]
+    int r;
+    float gamma;
+    float *part_val;    // [M][N/16]
+    int32_t *part_idx;  // [M][N/16]
+};
+void launch_gemm(DType t, Epi e, const GemmArgs &a, hipStream_t s);
+
+// y[m] = dtype(h[m] * rsqrt(mean(h[m]^2) + eps) * g), one row per workgroup.
+void launch_rmsnorm(DType t, const float *h, const float *g, int M, int d, float eps, void *y,
+                    hipStream_t s);
+
+// h[b*c + i] = E[tok[b * tok_stride + i]] as fp32.
+void launch_embed(DType t, const void *emb, const int32_t *tok, int tok_stride, int B, int c, int d,
+                  float *h, hipStream_t s);
+
+// dst[r] = src[r] for rows r in [0,M) with given row strides (fp32 rows of d).
+void launch_copy_rows(const float *src, int src_stride_rows, float *dst, int dst_stride_rows, int M,
+                      int d, hipStream_t s);
+
+// ctx rows: dst[(b*dst_rows_per_b + dst_off)*d .. ] = src[b*d ..]  (bytes-agnostic, elem bytes es)
+void launch_scatter_rows(const void *src, void *dst, int B, int d, int es, int dst_rows_per_b,
+                         int dst_off, hipStream_t s);
+
+struct AttnArgs {
+    const float *Q;      // [M][n_heads*hd]
+    const void *Kc, *Vc; // [max_batch][n_kv][s_max][hd]
+    const int32_t *lens;
+    int B, c, pos_off;
+    int n_heads, n_kv, hd, s_max;
+    int n_chunks;        // chunks of the longest context in this call
+    int chunk_stride;    // partial slots per (token, head) = ceil(s_max / 64)
+    float scale;
+    float *part_o;       // [M][n_heads][chunk_stride][hd]
+    float *part_ml;      // [M][n_heads][chunk_stride][2]
+    void *O;             // [M][n_heads*hd] out (dtype)
+};
+void launch_attention(DType t, const AttnArgs &a, hipStream_t s);
+
+// u[m][c] = sum_i B[c][i] * x[m][i]   (x dtype, B fp32 [r][d])
+void launch_lora_u(DType t, const void *x, const float *Bm, int M, int d, int r, float *u, hipStream_t s);
+
+// Per-row argmax over the per-tile partials (ties -> lowest id).  out[m * out_stride] =
+// forced ? forced[m * out_stride] : argmax; flags[0] |= 1 on non-finite logits.
+void launch_argmax(const float *part_val, const int32_t *part_idx, int M, int ntiles, int32_t *out,
+                   int out_stride, const int32_t *forced, int32_t *flags, hipStream_t s);
+
+struct CommitArgs {
+    int B, k_spec;
+    const int32_t *drafts;    // [B][k_spec]
+    const int32_t *targets;   // [B][k_spec]
+    const int32_t *max_new;   // [B] or nullptr
+    int32_t *lens, *pending;  // [B]
+    int32_t *tokens_out;      // [B][k_spec]
+    int32_t *n_out, *m_out;   // [B]
+    const int32_t *flags;     // [0] != 0: non-finite logits -> commit nothing
+    // replay ring
+    int32_t *ring_state;      // [0] next row, [1] valid rows
+    int ring_rows;
+    int32_t *copy_list;       // [B*k_spec][2]: (source row b*k_spec+i-1, ring slot), count at [-1]
+    int32_t *ring_a, *ring_i, *ring_prev;
+    int8_t *ring_r, *ring_fresh;
+};
+void launch_commit(const CommitArgs &a, hipStream_t s);
+
+// Copy the rows named by the commit's copy list into the ring (h_hat rows and verify logits).
+void launch_ring_copy(const int32_t *copy_list, int max_rows, const void *hk_hat, int d, int es,
+                      const float *vlogits, int V, void *ring_h, float *ring_logits, hipStream_t s);
+
+// ---- drafter update (Section 3.4) ----
+struct UpdateArgs {
+    const void *W;          // packed lm_head [V][d]
+    const void *Hh;         // ring h_hat [rows][d] (dtype)
+    const float *logits;    // ring logits^phi [rows][V]
+    const int32_t *a;       // [rows]
+    const int8_t *r, *fresh;
+    int n, V, d, rank;
+    float gamma, tau, baseline, c_kl, c_ce, c_pg, c_ent;
+    const float *A, *Bm;    // A_s [V][r], B_s [r][d]
+    float *u;               // [n][r]
+    float *Z;               // [n][V] drafter logits -> overwritten by g = dL/dz
+    float *part_val;        // scratch for the logits GEMM epilogue
+    int32_t *part_idx;
+    float *row_stats;       // [n][8]
+    float *dA;              // [V][r]
+    float *du;              // [n][r]
+    float *dB;              // [r][d]
+    float *loss_out;        // [16]: loss, kl, ce, pg, entropy, n, n_acc, n_fresh, n_fresh_acc | counts at [12..16)
+};
+void launch_update_forward(DType t, const UpdateArgs &u, hipStream_t s);
+void launch_update_backward(DType t, const UpdateArgs &u, hipStream_t s);
+void launch_adam(float *p, const float *g, float *m, float *v, int n, float lr, float b1, float b2,
+                 float eps, int step, hipStream_t s);
+
+}  // namespace dvi

@@ -1,0 +1,285 @@
+"""GPU parity: the HIP decode step against the CPU oracle, through the C ABI.
+
+Expected values come from tests/golden/*.npz (written by tests/golden/make_golden.py, which
+calls only the oracle) or from the oracle directly for small cases."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from oracle import dvi as odvi
+from oracle import update as oupd
+from tests import gpu_util as gu
+
+pytestmark = pytest.mark.gpu
+
+SMALL = ["tiny", "1b_L4", "7b_L4", "13b_L4"]
+KSPEC = {"tiny": 4, "1b_L4": 5, "7b_L4": 4, "13b_L4": 6}
+
+
+def _say(msg):
+    print(msg, flush=True)
+
+
+@pytest.mark.parametrize("name", SMALL)
+def test_free_running_tokens_match_oracle(name):
+    g = gu.golden(name)
+    shape = gu.SHAPES[name]
+    P, T = g["prompt"].size, g["tokens"].size
+    _say("free-running %s P=%d T=%d k_spec=%d" % (name, P, T, KSPEC[name]))
+    eng, _ = gu.engine(shape, max_seq=P + T + 16)
+    toks, info = eng.generate(g["prompt"][None], T, KSPEC[name])
+    agree = gu.compare_free_running(toks[0], g["tokens"], g["gaps"])
+    _say("  %d/%d tokens agree before the first (near-tie) divergence; mean m %.2f" % (agree, T, info["m"].mean()))
+    assert agree >= 1
+    eng.close()
+
+
+@pytest.mark.parametrize("name", SMALL)
+def test_teacher_forced_logits_and_argmax(name):
+    """Drafts and commits follow the oracle's sequence: every verify row's logits are within
+    the storage type's tolerance and its argmax matches wherever the oracle is not near a tie."""
+    g = gu.golden(name)
+    shape = gu.SHAPES[name]
+    P, T = g["prompt"].size, g["tokens"].size
+    R = g["logits"].shape[0]
+    _say("teacher-forced %s rows=%d" % (name, R))
+    eng, _ = gu.engine(shape, max_seq=P + T + 16)
+    rows = gu.teacher_forced(eng, g["prompt"], g["tokens"], KSPEC[name], R)
+    assert len(rows) == R
+    worst = 0.0
+    for idx, lg, am in rows:
+        e = gu.rel_l2(lg, g["logits"][idx])
+        worst = max(worst, e)
+        assert e <= gu.tol(shape), "row %d: relative L2 error %.3g" % (idx, e)
+        if g["gaps"][idx] > gu.TIE_GAP:
+            assert am == g["tokens"][idx], "row %d argmax %d != oracle %d" % (idx, am, g["tokens"][idx])
+    _say("  worst relative L2 logits error %.3g" % worst)
+    eng.close()
+
+
+def _gpu_run(eng, prompt, n_new, k_spec, forced_fn=None):
+    """Drive the ABI step by step; returns tokens and the per-step (drafts, targets, m, n)."""
+    first = eng.prefill(prompt[None])
+    out = [int(first[0])]
+    steps = []
+    while len(out) < n_new:
+        forced = forced_fn(out) if forced_fn else None
+        d = eng.draft(k_spec, forced=forced, want=True)
+        tg, mv = eng.verify(want=True)
+        tok, n, m = eng.commit(max_new=np.array([n_new - len(out)], np.int32))
+        assert m[0] == mv[0]
+        out.extend(int(t) for t in tok[0, :n[0]])
+        steps.append((d[0].copy(), tg[0].copy(), int(m[0]), int(n[0])))
+    return np.array(out, np.int32), steps
+
+
+@pytest.mark.parametrize("name", ["tiny", "7b_L4"])
+def test_dvi_equals_gpu_greedy_and_kv_rollback_bitwise(name):
+    """(R3) speculative decoding equals plain greedy decoding on the same engine, token for
+    token, with bitwise-equal committed keys/values; (R2) two runs that differ only in which
+    wrong drafts were proposed end bitwise equal; (R1) a rejected step leaves KV[0, len) as is."""
+    shape = gu.SHAPES[name]
+    P, T = 70, 30
+    prompt = synth.make_prompts(shape.vocab, 1, P, 3)[0]
+    eng, w = gu.engine(shape, max_seq=P + T + 16)
+    ar, _ = _gpu_run(eng, prompt, T, 1)
+    Lc = P + T - 1
+    kv_ar = [eng.read_kv(l, 0, 0, Lc) for l in range(shape.n_layers)]
+    spec, steps = _gpu_run(eng, prompt, T, 4)
+    assert np.array_equal(spec, ar)
+    assert eng.lengths()[0] == Lc
+    for l in range(shape.n_layers):
+        k, v = eng.read_kv(l, 0, 0, Lc)
+        assert np.array_equal(k, kv_ar[l][0]) and np.array_equal(v, kv_ar[l][1]), "layer %d" % l
+    rng1, rng2 = np.random.default_rng(1), np.random.default_rng(2)
+    r1, _ = _gpu_run(eng, prompt, T, 4, lambda out: rng1.integers(0, shape.vocab, (1, 4)))
+    kv1 = [eng.read_kv(l, 0, 0, Lc) for l in range(shape.n_layers)]
+    r2, _ = _gpu_run(eng, prompt, T, 4, lambda out: rng2.integers(0, shape.vocab, (1, 4)))
+    assert np.array_equal(r1, ar) and np.array_equal(r2, ar)
+    for l in range(shape.n_layers):
+        k, v = eng.read_kv(l, 0, 0, Lc)
+        assert np.array_equal(k, kv1[l][0]) and np.array_equal(v, kv1[l][1])
+    # R1: one step of all-wrong drafts: KV[0, len) untouched, one token committed
+    eng.prefill(prompt[None])
+    before = [eng.read_kv(l, 0, 0, P) for l in range(shape.n_layers)]
+    wrong = (ar[1:5] + 1) % shape.vocab
+    eng.draft(4, forced=wrong[None])
+    eng.verify()
+    tok, n, m = eng.commit()
+    assert m[0] == 0 and n[0] == 1 and tok[0, 0] == ar[1]
+    for l in range(shape.n_layers):
+        k, v = eng.read_kv(l, 0, 0, P)
+        assert np.array_equal(k, before[l][0]) and np.array_equal(v, before[l][1])
+    eng.close()
+
+
+@pytest.mark.parametrize("j", [0, 1, 2, 3, 4])
+def test_every_accept_length_and_replay_rows(j):
+    shape = gu.SHAPES["tiny"]
+    P, T, k = 40, 26, 4
+    prompt = synth.make_prompts(shape.vocab, 1, P, 5)[0]
+    eng, _ = gu.engine(shape, max_seq=P + T + 16)
+    ar, _ = _gpu_run(eng, prompt, T, 1)
+
+    def forced(out):
+        nxt = ar[len(out):len(out) + k].copy()
+        if nxt.size < k:
+            nxt = np.concatenate([nxt, np.zeros(k - nxt.size, np.int32)])
+        if j < k:
+            nxt[j] = (nxt[j] + 1) % shape.vocab
+        return nxt[None]
+
+    toks, steps = _gpu_run(eng, prompt, T, k, forced)
+    assert np.array_equal(toks, ar)
+    full = [s for s in steps[:-1]]
+    assert all(s[2] == j for s in full), [s[2] for s in steps]
+    valid, nxt = eng.buffer_info()
+    expect_rows = sum(min(s[2] + 1, k) for s in steps)
+    assert valid == min(expect_rows, 256)
+    buf = eng.read_buffer(0, valid)
+    row = 0
+    for d, tg, m, n in steps:
+        cnt = min(m + 1, k)
+        assert list(buf["r"][row:row + cnt]) == [1] * min(m, k) + ([0] if m < k else [])
+        assert list(buf["a"][row:row + cnt]) == list(d[:cnt])
+        assert list(buf["i"][row:row + cnt]) == list(range(1, cnt + 1))
+        assert all(buf["fresh"][row:row + cnt] == 1)
+        row += cnt
+    eng.close()
+
+
+def test_buffer_rows_hold_the_verify_logits_and_normed_states():
+    shape = gu.SHAPES["tiny"]
+    g = gu.golden("tiny")
+    eng, w = gu.engine(shape, max_seq=128)
+    eng.prefill(g["prompt"][None])
+    eng.draft(4)
+    eng.verify()
+    lg = eng.read_logits()[0]
+    tok, n, m = eng.commit()
+    buf = eng.read_buffer(0, min(m[0] + 1, 4))
+    for i in range(buf["a"].size):
+        assert np.array_equal(buf["logits"][i], lg[i])
+    # h rows are RMSNorm(h_k) with unit gain: mean square 1 up to eps
+    ms = (buf["h"].astype(np.float64) ** 2).mean(axis=1)
+    assert np.allclose(ms, 1.0, atol=1e-4)
+    eng.close()
+
+
+@pytest.mark.parametrize("name,n_rows", [("tiny", 48), ("1b_L4", 200)])
+def test_drafter_update_gradients_match_oracle(name, n_rows):
+    shape = gu.SHAPES[name]
+    eng, w = gu.engine(shape, max_seq=64, lora_A_std=0.02)
+    buf = synth.make_buffer(shape.d_model, shape.vocab, n_rows, seed=11)
+    eng.prefill(synth.make_prompts(shape.vocab, 1, 8, 1))
+    eng.write_buffer(buf.h, buf.a, buf.logits, buf.r, buf.fresh)
+    c = oupd.Coeffs(c_kl=0.7, c_ce=0.9, c_pg=0.4, c_ent=0.05, tau=1.3, baseline=0.35)
+    st = eng.update_drafter(c.c_kl, c.c_ce, c.c_pg, c.c_ent, c.tau, c.baseline, lr=0.0, grads=True)
+    W = w.as_f32(w.lm_head).astype(np.float64)
+    ref = oupd.loss_and_grad(W, w.lora_A.astype(np.float64), w.lora_B.astype(np.float64), shape.lora_gamma,
+                             buf.h.astype(np.float64), buf.a, buf.logits, buf.r, buf.fresh, c)
+    dA = st["grad_A"].cpu().numpy()
+    dB = st["grad_B"].cpu().numpy()
+    eA, eB = gu.rel_l2(dA, ref.dA), gu.rel_l2(dB, ref.dB)
+    _say("update %s rows=%d: |dA| rel err %.3g, |dB| rel err %.3g, loss %.6g vs %.6g"
+         % (name, n_rows, eA, eB, st["loss"], ref.loss))
+    assert eA <= 1e-2 and eB <= 1e-2
+    assert st["rows"] == n_rows and st["accepted"] == int(buf.r.sum()) and st["fresh"] == int(buf.fresh.sum())
+    for key in ("kl", "ce", "pg", "entropy"):
+        assert abs(st[key] - getattr(ref, key)) <= 1e-3 * max(1.0, abs(getattr(ref, key))), key
+    # an Adam step with lr > 0 moves A_s, B_s as the oracle's Adam does (same gradient)
+    A0, B0 = eng.lora_A.cpu().numpy().copy(), eng.lora_B.cpu().numpy().copy()
+    eng.update_drafter(c.c_kl, c.c_ce, c.c_pg, c.c_ent, c.tau, c.baseline, lr=1e-3, opt_step=1)
+    A1, B1 = eng.lora_A.cpu().numpy(), eng.lora_B.cpu().numpy()
+    # the fresh flags were cleared by the first update: recompute the oracle gradient without them
+    ref2 = oupd.loss_and_grad(W, A0.astype(np.float64), B0.astype(np.float64), shape.lora_gamma,
+                              buf.h.astype(np.float64), buf.a, buf.logits, buf.r, np.zeros_like(buf.fresh), c)
+    z = np.zeros_like(A0, np.float64)
+    Ae, _, _ = oupd.adam_step(A0.astype(np.float64), ref2.dA, z, z.copy(), 1, 1e-3)
+    zb = np.zeros_like(B0, np.float64)
+    Be, _, _ = oupd.adam_step(B0.astype(np.float64), ref2.dB, zb, zb.copy(), 1, 1e-3)
+    assert gu.rel_l2(A1 - A0, Ae - A0) <= 5e-2 and gu.rel_l2(B1 - B0, Be - B0) <= 5e-2
+    eng.close()
+
+
+def test_batched_sequences_are_independent():
+    """Batch of 4 equals four single-sequence runs, token for token and bitwise in KV."""
+    shape = gu.SHAPES["7b_L4"]
+    P, T, B = 40, 20, 4
+    prompts = synth.make_prompts(shape.vocab, B, P, 9)
+    w = synth.make_weights(shape, 0)
+    eng, _ = gu.engine(shape, max_batch=B, max_seq=P + T + 16, weights=w)
+    toks, info = eng.generate(prompts, T, 4)
+    kvb = [eng.read_kv(1, b, 0, P + 5) for b in range(B)]
+    eng.close()
+    eng1, _ = gu.engine(shape, max_batch=1, max_seq=P + T + 16, weights=w)
+    for b in range(B):
+        t1, _ = eng1.generate(prompts[b:b + 1], T, 4)
+        assert np.array_equal(t1[0], toks[b]), b
+        k, v = eng1.read_kv(1, 0, 0, P + 5)
+        assert np.array_equal(k, kvb[b][0]) and np.array_equal(v, kvb[b][1])
+    eng1.close()
+
+
+def test_run_to_run_determinism():
+    shape = gu.SHAPES["1b_L4"]
+    prompt = synth.make_prompts(shape.vocab, 1, 50, 4)
+    eng, _ = gu.engine(shape, max_seq=100)
+    a, ia = eng.generate(prompt, 24, 5)
+    la = eng.read_logits().copy()
+    b, ib = eng.generate(prompt, 24, 5)
+    lb = eng.read_logits()
+    assert np.array_equal(a, b) and np.array_equal(la, lb)
+    assert np.array_equal(ia["m"], ib["m"])
+    eng.close()
+
+
+def test_state_capacity_and_numeric_errors():
+    from paper_2510_05421_amd._abi import DVIError, ERR_STATE, ERR_CAPACITY, ERR_ARG, ERR_NUMERIC
+    shape = gu.SHAPES["tiny"]
+    w = synth.make_weights(shape, 0)
+    eng, _ = gu.engine(shape, max_seq=48, max_k_spec=4, weights=w)
+    with pytest.raises(DVIError) as e:
+        eng.draft(2)
+    assert e.value.status == ERR_STATE
+    eng.prefill(synth.make_prompts(shape.vocab, 1, 40, 0))
+    with pytest.raises(DVIError) as e:
+        eng.verify()
+    assert e.value.status == ERR_STATE
+    with pytest.raises(DVIError) as e:
+        eng.draft(5)
+    assert e.value.status == ERR_CAPACITY
+    with pytest.raises(DVIError) as e:
+        eng.draft(4, forced=np.array([[1, 2, 3, shape.vocab]]))
+    assert e.value.status == ERR_ARG
+    eng.draft(4)
+    eng.abort()                          # back to READY; lengths unchanged
+    assert eng.lengths()[0] == 40
+    eng.draft(4)
+    eng.verify()
+    tok, n, m = eng.commit()
+    L = 40 + int(n[0])
+    while L + 4 <= 48:
+        eng.draft(4)
+        eng.verify()
+        tok, n, m = eng.commit()
+        L += int(n[0])
+    with pytest.raises(DVIError) as e:   # len + k_spec > max_seq
+        eng.draft(4)
+    assert e.value.status == ERR_CAPACITY
+    eng.close()
+    # a NaN in the head makes the head's logits non-finite: the commit refuses, abort recovers
+    w.lm_head = w.lm_head.copy()
+    w.lm_head[7, 3] = np.nan
+    eng, _ = gu.engine(shape, max_seq=64, weights=w)
+    with pytest.raises(DVIError) as e:
+        eng.prefill(synth.make_prompts(shape.vocab, 1, 8, 0))
+    assert e.value.status == ERR_NUMERIC
+    eng.draft(2)
+    eng.verify()
+    with pytest.raises(DVIError) as e:
+        eng.commit()
+    assert e.value.status == ERR_NUMERIC
+    eng.abort()
+    eng.close()
