@@ -1,0 +1,246 @@
+#!/usr/bin/env python3
+"""Benchmark of DVI's self-speculative decode step on one MI355X.
+
+A step is one pass of the whole hot path for every sequence of the batch: k_spec serial
+drafts through layers 1..k plus the LoRA draft head, one block verify through layers
+k+1..L plus the frozen head, the commit (longest agreeing prefix, KV rollback, replay
+logging) and, on workloads that train the drafter, the periodic drafter update.  The
+prompt is prefilled before timing; weights, KV cache and prompt are resident in HBM.
+
+Prints ONE JSON line: committed tokens/s of the whole job (value), ms per step, the
+verify-step and draft-token HBM bandwidth from HIP events, the roofline of the dominant
+kernel (its algorithmic bytes per launch over its HIP-event duration), acceptance
+statistics, the same engine decoding plainly (k_spec = 1) for the speedup ratio, and the
+CPU oracle timed on the host cores on a bounded sample of the same workload.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 7b] [--k-spec 4]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0     # MI355X HBM3E, published
+METRIC = "committed tokens/s (7B shape, bs=1) + verify-step HBM GB/s vs peak"
+PAPER_CONTEXT = ("paper: 2.16x average wall-time speedup over greedy AR decoding on 1x NVIDIA H100 "
+                 "(Vicuna-7B, Spec-Bench, split k=2, k_spec=4); no absolute tokens/s published")
+KERNEL_NAMES = {"gate_up": "gemm_kernel<bf16,MG=1,EPI_SWIGLU> (gate/up projection, SwiGLU epilogue)",
+                "qkv": "gemm_kernel<bf16,MG=1,EPI_QKV>", "down": "gemm_kernel<bf16,MG=1,EPI_RESID> (MLP down)",
+                "head": "gemm_kernel<bf16,MG=1,EPI_LOGITS>", "attention": "attn_partial+attn_combine"}
+
+
+def log(msg):
+    print("[bench] " + msg, file=sys.stderr, flush=True)
+
+
+def algorithmic_bytes(shape, layers, rows_per_seq, lens, head_rows, lora=False):
+    """Bytes a pass must move: each weight once, keys/values read over the context and
+    written for the new rows, the head logits written.  rows_per_seq tokens per sequence."""
+    es = 2 if shape.bf16 else 4
+    w = layers * shape.layer_params() * es + shape.vocab * shape.d_model * es
+    if lora:
+        w += shape.vocab * shape.lora_rank * 4 + shape.lora_rank * shape.d_model * 4
+    kv = 0
+    for L0 in lens:
+        kv += layers * (L0 + rows_per_seq) * shape.kv_dim * 2 * es   # read 0..len+rows-1 (incl. new)
+    return w + kv + head_rows * shape.vocab * 4
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=None)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="7b")
+    ap.add_argument("--k-spec", type=int, default=None)
+    ap.add_argument("--probe", default="gate_up", choices=sorted(KERNEL_NAMES))
+    ap.add_argument("--probe-steps", type=int, default=20)
+    ap.add_argument("--ar-steps", type=int, default=40)
+    ap.add_argument("--cpu-seconds", type=float, default=20.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-ar", action="store_true")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build runs the decode step on a single MI355X "
+              "(no multi-GPU path); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import synth
+    from paper_2510_05421_amd.engine import Engine, EngineConfig
+
+    wl = synth.WORKLOADS[args.workload]
+    shape = wl.model
+    k = args.k_spec or wl.k_spec[0]
+    B, P, N = wl.batch, wl.prompt_len, wl.new_tokens
+    W = args.warmup
+    K = args.steps if args.steps is not None else max(1, min(100, (N - 1) // k - W))
+    if (W + K) * k >= N:
+        sys.exit("warmup+steps (%d) x k_spec (%d) exceeds the workload's %d new tokens" % (W + K, k, N))
+
+    log("workload %s: generating weights" % wl.name)
+    t = time.time()
+    w = synth.make_weights(shape, 0)
+    prompts = synth.make_prompts(shape.vocab, B, P, 0)
+    log("weights ready in %.1f s; building engine" % (time.time() - t))
+    cfg = EngineConfig.from_shape(shape, max_batch=B, max_seq=P + N + 2 * k + 2, max_k_spec=max(k, 8),
+                                  buffer_rows=wl.buffer_rows)
+    eng = Engine(cfg, w, "cuda:0")
+    from paper_2510_05421_amd.schedule import KLRLSchedule
+    sched = KLRLSchedule()
+
+    remaining = np.full(B, N - 1, np.int32)
+    state = {"step": 0}
+
+    def step(kk, stats=None, update=True):
+        lens_before = eng_lens[:]
+        eng.draft(kk)
+        eng.verify()
+        tok, n, m = eng.commit(max_new=remaining)
+        remaining[:] = remaining - n
+        for b in range(B):
+            eng_lens[b] += int(n[b])
+        state["step"] += 1
+        if update and wl.update_every and kk > 1 and state["step"] % wl.update_every == 0:
+            c = sched.coeffs(eng.updates, eng.baseline)
+            st = eng.update_drafter(c["c_kl"], c["c_ce"], c["c_pg"], c["c_ent"], c["tau"], eng.baseline, lr=1e-3)
+            if st["fresh"] > 0:
+                eng.baseline = sched.ema(eng.baseline, st["fresh_accepted"] / st["fresh"])
+            eng.updates += 1
+        if stats is not None:
+            tm = eng.timings()
+            stats["tokens"] += int(n.sum())
+            stats["m"].append(m.copy())
+            stats["n"].append(n.copy())
+            stats["verify_ms"].append(tm["verify"])
+            stats["draft_ms"].append(tm["draft"])
+            stats["verify_bytes"].append(algorithmic_bytes(shape, shape.n_layers - shape.split_k, kk,
+                                                           lens_before, B * kk))
+            stats["draft_bytes"].append(sum(algorithmic_bytes(shape, shape.split_k, 1,
+                                                              [l0 + j for l0 in lens_before], B, lora=True)
+                                            for j in range(kk)))
+
+    log("prefill %d x %d tokens" % (B, P))
+    t = time.time()
+    eng.prefill(prompts)
+    torch.cuda.synchronize()
+    log("prefill %.2f s" % (time.time() - t))
+    eng_lens = [P] * B
+    for _ in range(W):
+        step(k)
+    st = {"tokens": 0, "m": [], "n": [], "verify_ms": [], "draft_ms": [], "verify_bytes": [], "draft_bytes": []}
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(K):
+        step(k, st)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    elapsed = t1 - t0
+    value = st["tokens"] / elapsed
+    ms_step = 1e3 * elapsed / K
+    mv = np.array(st["m"])
+    nv = np.array(st["n"])
+    ver_ms = float(np.median(st["verify_ms"]))
+    ver_gbs = float(np.mean(st["verify_bytes"])) / (ver_ms * 1e-3) / 1e9
+    dr_ms = float(np.median(st["draft_ms"]))
+    dr_gbs = float(np.mean(st["draft_bytes"])) / (dr_ms * 1e-3) / 1e9
+    log("timed %d steps: %.1f tokens/s, %.2f ms/step, mean m %.2f, verify %.3f ms (%.0f GB/s), "
+        "draft %.3f ms (%.0f GB/s)" % (K, value, ms_step, mv.mean(), ver_ms, ver_gbs, dr_ms, dr_gbs))
+
+    # dominant kernel: every launch of one kernel class timed with HIP events on the engine's stream
+    # (a sequence that has all its tokens keeps computing with its commits masked, so the
+    # kernel sees the same shapes whether or not the probe pass runs past the last token)
+    roof = None
+    if args.probe_steps > 0:
+        eng.probe(args.probe)
+        for _ in range(args.probe_steps):
+            step(k, update=False)
+        pr = eng.probe_read()
+        eng.probe("off")
+        if pr["launches"]:
+            avg_ms = pr["ms"] / pr["launches"]
+            per_launch = pr["bytes"] / pr["launches"]
+            achieved = per_launch / (avg_ms * 1e-3) / 1e9
+            roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                    "kernel": KERNEL_NAMES[args.probe], "launches": pr["launches"],
+                    "avg_us": round(avg_ms * 1e3, 2), "bytes_per_launch": int(per_launch)}
+            log("probe %s: %d launches, avg %.1f us, %.0f GB/s" % (args.probe, pr["launches"], avg_ms * 1e3,
+                                                                  achieved))
+
+    ar = None
+    if not args.no_ar:
+        eng.prefill(prompts)
+        remaining[:] = N - 1
+        eng_lens[:] = [P] * B
+        for _ in range(W):
+            step(1)
+        sa = {"tokens": 0, "m": [], "n": [], "verify_ms": [], "draft_ms": [], "verify_bytes": [], "draft_bytes": []}
+        KA = min(args.ar_steps, N - 1 - W)
+        torch.cuda.synchronize()
+        a0 = time.perf_counter()
+        for _ in range(KA):
+            step(1, sa)
+        torch.cuda.synchronize()
+        a1 = time.perf_counter()
+        ar_tps = sa["tokens"] / (a1 - a0)
+        ar = {"tokens_per_s": round(ar_tps, 2), "steps": KA, "speedup": round(value / ar_tps, 3)}
+        log("plain AR on the same engine: %.1f tokens/s -> speedup %.2fx" % (ar_tps, value / ar_tps))
+    eng.close()
+    del eng
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        from oracle import dvi as odvi
+        cores = int(os.environ.get("OMP_NUM_THREADS", len(os.sched_getaffinity(0))))
+        om = oracle.OracleModel(w)
+        prefix = 16
+        drafter = odvi.Drafter(w.lora_A.astype(np.float64), w.lora_B.astype(np.float64), shape.lora_gamma)
+        # one step first to size the bounded sample, then enough steps for ~cpu_seconds
+        c0 = time.perf_counter()
+        r = odvi.dvi_generate(om, prompts[0, :prefix], 1 + 8 * k, k, drafter, max_steps=1)
+        one = time.perf_counter() - c0
+        steps = max(1, int(args.cpu_seconds / max(one, 1e-3)))
+        c0 = time.perf_counter()
+        r = odvi.dvi_generate(om, prompts[0, :prefix], 1 + steps * k, k, drafter, max_steps=steps)
+        c1 = time.perf_counter()
+        committed = len(r.tokens) - 1
+        cpu = {"value": round(committed / (c1 - c0), 4), "unit": "tokens/s", "cores": cores, "kind": "oracle",
+               "sample": "float64 oracle DVI rollout (k_spec=%d) of the same model, one sequence, %d-token prefix "
+                         "of the workload prompt (prefill included), %d steps, %d committed tokens in %.1f s"
+                         % (k, prefix, len(r.steps), committed, c1 - c0)}
+        log("cpu oracle: %s" % cpu["sample"])
+
+    dt = "bf16" if shape.bf16 else "f32"
+    out = {
+        "metric": METRIC, "value": round(value, 3), "unit": "tokens/s", "n_gpus": 1, "steps": K, "warmup": W,
+        "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": dt, "data": "synthetic",
+        "config": {"workload": "%s: %dL split k=%d, d=%d, %dx%d heads (%d kv), SwiGLU %d, vocab %d, %s; "
+                               "batch %d, %d-token random prompt, %d new tokens, k_spec=%d"
+                               % (wl.name, shape.n_layers, shape.split_k, shape.d_model, shape.n_heads,
+                                  shape.head_dim, shape.n_kv_heads, shape.ffn_dim, shape.vocab, dt, B, P, N, k),
+                   "batch": B, "prompt_len": P, "new_tokens": N, "k_spec": k, "split_k": shape.split_k},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "verify_step": {"ms": round(ver_ms, 4), "gb_s": round(ver_gbs, 1), "frac": round(ver_gbs / HBM_PEAK_GBS, 4),
+                        "bytes": int(np.mean(st["verify_bytes"]))},
+        "draft_token": {"ms": round(dr_ms / k, 4), "gb_s": round(dr_gbs, 1), "frac": round(dr_gbs / HBM_PEAK_GBS, 4)},
+        "acceptance": {"mean_m": round(float(mv.mean()), 4), "mean_tokens_per_step": round(float(nv.mean()), 4),
+                       "rate": round(float(mv.mean()) / k, 4)},
+        "ar_baseline": ar,
+        "paper_context": PAPER_CONTEXT,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -115,13 +115,15 @@ class Drafter:
 def dvi_generate(model: OracleModel, prompt, n_new: int, k_spec: int, drafter: Drafter,
                  forced_drafts: Optional[Callable[[int, int, np.ndarray], Optional[np.ndarray]]] = None,
                  on_step: Optional[Callable[["DVIResult", int], None]] = None,
-                 s_max: Optional[int] = None, split_k: Optional[int] = None) -> DVIResult:
+                 s_max: Optional[int] = None, split_k: Optional[int] = None,
+                 max_steps: Optional[int] = None) -> DVIResult:
     """Run DVI draft -> verify -> commit -> log until n_new tokens are committed.
 
     forced_drafts(step, pos, committed) may return an int array [k_spec] that
     replaces the drafter's argmax (test hook for exercising every m).
     on_step(result, step) is called after each commit; it may replace
     drafter.A / drafter.B (the online update), read at the next draft.
+    max_steps stops after that many decode steps (bounded runs).
     """
     s = model.shape
     k = s.split_k if split_k is None else split_k
@@ -135,7 +137,7 @@ def dvi_generate(model: OracleModel, prompt, n_new: int, k_spec: int, drafter: D
     length = P                   # tokens whose keys/values are in the cache
     res = DVIResult(np.zeros(0, np.int32), [], [], cache, length)
     step = 0
-    while len(out) < n_new:
+    while len(out) < n_new and (max_steps is None or step < max_steps):
         # ---- draft: k_spec serial single-token passes through layers 1..k
         tau = [out[-1]]
         hk_rows, drafts = [], []
