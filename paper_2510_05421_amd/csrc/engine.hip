@@ -55,9 +55,12 @@ struct dvi_ctx {
     float *final_norm;
     float2 *rope;
     float *lora_A, *lora_B;
-    // activations
-    float *h, *q, *hk, *vlogits, *dlogits, *part_val, *att_po, *att_pml, *lora_u;
-    void *xn, *attn_o, *act, *hk_hat;
+    // activations.  Residual stream h (fp32) travels with its per-16-column sums of squares
+    // (ss) and dtype(h * g) for the next folded RMSNorm (hg); hk/hk_ss/hk_hg hold the k_spec
+    // drafted rows of every sequence (row b*k_spec + j), which the verify then continues.
+    // GEMM inputs (hg, act, attn_o, hk_hg, dfm, pfm, ufm) are in the fragment-major layout.
+    float *h, *ss, *q, *hk, *hk_ss, *vlogits, *dlogits, *part_val, *att_po, *att_pml, *lora_u;
+    void *hg, *attn_o, *act, *hk_hg, *hk_hat, *dfm, *pfm, *ufm;
     int32_t *part_idx;
     // small device state; io block is one contiguous region copied back at commit
     int32_t *lens, *pending, *drafts, *targets, *forced, *max_new, *ids, *copy_list, *ring_state;
@@ -147,13 +150,21 @@ static size_t layout(dvi_ctx *x, const dvi_config &c, void *base) {
     void *head = b.take<void>(V * d * es);
     float *final_norm = b.take<float>(d * 4);
     float2 *rope = b.take<float2>((size_t)c.max_seq * (c.head_dim / 2) * 8);
+    const size_t nps = d / 16;
+    const size_t M16 = (M + 15) / 16 * 16, Bk16 = (Bk + 15) / 16 * 16, B16 = ((size_t)c.max_batch + 15) / 16 * 16;
     float *h = b.take<float>(M * d * 4);
-    void *xn = b.take<void>(M * d * es);
+    float *ss = b.take<float>(M * nps * 4);
+    void *hg = b.take<void>(M16 * d * es);
     float *q = b.take<float>(M * qd * 4);
-    void *attn_o = b.take<void>(M * qd * es);
-    void *act = b.take<void>(M * F * es);
+    void *attn_o = b.take<void>(M16 * qd * es);
+    void *act = b.take<void>(M16 * F * es);
     float *hk = b.take<float>(Bk * d * 4);
+    float *hk_ss = b.take<float>(Bk * nps * 4);
+    void *hk_hg = b.take<void>(Bk16 * d * es);
     void *hk_hat = b.take<void>(Bk * d * es);
+    void *dfm = b.take<void>(B16 * d * es);
+    void *pfm = b.take<void>(B16 * d * es);
+    void *ufm = b.take<void>((size_t)64 * d * es);
     float *vlogits = b.take<float>(M * V * 4);
     float *dlogits = b.take<float>((size_t)c.max_batch * V * 4);
     float *part_val = b.take<float>(M * (V / 16) * 4);
@@ -195,7 +206,9 @@ static size_t layout(dvi_ctx *x, const dvi_config &c, void *base) {
     if (x && base) {
         x->L = Ls;
         x->emb = emb; x->head = head; x->final_norm = final_norm; x->rope = rope;
-        x->h = h; x->xn = xn; x->q = q; x->attn_o = attn_o; x->act = act; x->hk = hk; x->hk_hat = hk_hat;
+        x->h = h; x->ss = ss; x->hg = hg; x->q = q; x->attn_o = attn_o; x->act = act;
+        x->hk = hk; x->hk_ss = hk_ss; x->hk_hg = hk_hg; x->hk_hat = hk_hat;
+        x->dfm = dfm; x->pfm = pfm; x->ufm = ufm;
         x->vlogits = vlogits; x->dlogits = dlogits; x->part_val = part_val; x->part_idx = part_idx;
         x->att_po = att_po; x->att_pml = att_pml; x->lora_u = lora_u;
         x->lens = lens; x->pending = pending; x->drafts = drafts; x->targets = targets; x->forced = forced;
@@ -429,10 +442,20 @@ static void gemm(dvi_ctx *x, Epi e, int cls, const void *W, const void *X, int M
     if (pr) probe_end(x, gemm_bytes(x, e, M, N, K));
 }
 
-// Layers [l0, l1) on M = B*c rows of h; row b*c+i sits at position lens[b] + pos_off + i.
-static dvi_status run_layers(dvi_ctx *x, int l0, int l1, int B, int c, int pos_off, float *h) {
+// Layers [l0, l1) on M = B*c rows; row r = b*c+i sits at position lens[b] + pos_off + i.  The
+// fp32 residual stream and its sums of squares live at row r*rs of h / ss.  hg (FM, compact rows
+// r) holds dtype(h * attn_norm[l0]) on entry; the last layer's MLP-down epilogue writes
+// dtype(h * g) for the norm that follows layer l1-1 (attn_norm[l1], or final_norm at L) to FM row
+// r*out_rs + out_off of out_hg.
+static const float *next_gain(dvi_ctx *x, int l) {
+    return l + 1 < x->cfg.n_layers ? x->L[l + 1].attn_norm : x->final_norm;
+}
+
+static dvi_status run_layers(dvi_ctx *x, int l0, int l1, int B, int c, int pos_off, float *h, float *ss, void *hg,
+                             int rs, void *out_hg, int out_rs, int out_off) {
     const dvi_config &cf = x->cfg;
     const int d = cf.d_model, F = cf.ffn_dim, H = cf.n_heads, Hkv = cf.n_kv_heads, hd = cf.head_dim;
+    const int nps = d / 16;
     const int M = B * c;
     int pmax = 0;
     for (int b = 0; b < B; ++b) {
@@ -441,8 +464,10 @@ static dvi_status run_layers(dvi_ctx *x, int l0, int l1, int B, int c, int pos_o
     }
     for (int l = l0; l < l1; ++l) {
         const LayerW &Lw = x->L[l];
-        launch_rmsnorm(x->dt, h, Lw.attn_norm, M, d, cf.rms_eps, x->xn, x->stream);
         GemmArgs a{};
+        a.ss_in = ss;
+        a.ld_ss_in = rs * nps;
+        a.eps = cf.rms_eps;
         a.c = c;
         a.pos_off = pos_off;
         a.lens = x->lens;
@@ -454,7 +479,7 @@ static dvi_status run_layers(dvi_ctx *x, int l0, int l1, int B, int c, int pos_o
         a.hd = hd;
         a.s_max = cf.max_seq;
         a.rope = x->rope;
-        gemm(x, EPI_QKV, DVI_PROBE_QKV, Lw.wqkv, x->xn, M, qkv_rows(cf), d, a);
+        gemm(x, EPI_QKV, DVI_PROBE_QKV, Lw.wqkv, hg, M, qkv_rows(cf), d, a);
         AttnArgs at{};
         at.Q = x->q;
         at.Kc = Lw.Kc;
@@ -483,11 +508,26 @@ static dvi_status run_layers(dvi_ctx *x, int l0, int l1, int B, int c, int pos_o
         }
         GemmArgs r{};
         r.H = h;
+        r.ldh = rs * d;
+        r.ss_out = ss;
+        r.ld_ss_out = rs * nps;
+        r.hg_out = hg;
+        r.hg_rs = 1;
+        r.hg_off = 0;
+        r.g_next = Lw.mlp_norm;
         gemm(x, EPI_RESID, DVI_PROBE_ATTN_OUT, Lw.wo, x->attn_o, M, d, H * hd, r);
-        launch_rmsnorm(x->dt, h, Lw.mlp_norm, M, d, cf.rms_eps, x->xn, x->stream);
         GemmArgs g{};
+        g.ss_in = ss;
+        g.ld_ss_in = rs * nps;
+        g.eps = cf.rms_eps;
         g.A = x->act;
-        gemm(x, EPI_SWIGLU, DVI_PROBE_GATE_UP, Lw.wgu, x->xn, M, 2 * F, d, g);
+        gemm(x, EPI_SWIGLU, DVI_PROBE_GATE_UP, Lw.wgu, hg, M, 2 * F, d, g);
+        r.g_next = next_gain(x, l);
+        if (l == l1 - 1) {
+            r.hg_out = out_hg;
+            r.hg_rs = out_rs;
+            r.hg_off = out_off;
+        }
         gemm(x, EPI_RESID, DVI_PROBE_DOWN, Lw.wd, x->act, M, d, F, r);
     }
     LAUNCHCHK(x);
@@ -501,21 +541,25 @@ static int io_flags(const dvi_ctx *x) { return io_m(x) + x->cfg.max_batch; }
 static int io_words(const dvi_ctx *x) { return io_flags(x) + 4; }
 static int32_t *flags_ptr(dvi_ctx *x) { return x->io + io_flags(x); }
 
-// Vocabulary head on M normalised rows in x->xn: logits -> Z, argmax -> out (stride).
-static void head(dvi_ctx *x, int M, float *Z, bool lora, int32_t *out, int out_stride, const int32_t *forced) {
+// Vocabulary head on M rows of X (FM): logits -> Z, argmax -> out (stride).
+// ss_in != nullptr: X holds dtype(h * final_norm) and rows are scaled by 1/rms (folded norm).
+static void head(dvi_ctx *x, const void *X, const float *ss_in, int ld_ss, int M, float *Z, bool lora, int32_t *out,
+                 int out_stride, const int32_t *forced) {
     const dvi_config &cf = x->cfg;
     GemmArgs a{};
+    a.ss_in = ss_in;
+    a.ld_ss_in = ld_ss;
+    a.eps = cf.rms_eps;
     a.Z = Z;
     a.part_val = x->part_val;
     a.part_idx = x->part_idx;
     if (lora) {
-        launch_lora_u(x->dt, x->xn, x->lora_B, M, cf.d_model, cf.lora_rank, x->lora_u, x->stream);
         a.lora_A = x->lora_A;
         a.lora_u = x->lora_u;
         a.r = cf.lora_rank;
         a.gamma = cf.lora_gamma;
     }
-    gemm(x, EPI_LOGITS, DVI_PROBE_HEAD, x->head, x->xn, M, cf.vocab, cf.d_model, a);
+    gemm(x, EPI_LOGITS, DVI_PROBE_HEAD, x->head, X, M, cf.vocab, cf.d_model, a);
     launch_argmax(x->part_val, x->part_idx, M, cf.vocab / 16, out, out_stride, forced, flags_ptr(x), x->stream);
 }
 
@@ -560,15 +604,16 @@ extern "C" dvi_status dvi_prefill(dvi_ctx *x, int32_t batch, const int32_t *ids,
     x->B = batch;
     for (int b = 0; b < cf.max_batch; ++b) x->lens_h[b] = 0;
     const int c = (kMaxRows / batch) < 1 ? 1 : kMaxRows / batch;
+    const int nps = d / 16;
     for (int s0 = 0; s0 < P; s0 += c) {
         const int cc = (P - s0) < c ? P - s0 : c;
-        launch_embed(x->dt, x->emb, x->ids + s0, P, batch, cc, d, x->h, x->stream);
-        dvi_status st = run_layers(x, 0, cf.n_layers, batch, cc, s0, x->h);
+        launch_embed(x->dt, x->emb, x->ids + s0, P, batch, cc, d, x->h, d, x->ss, nps, x->hg, x->L[0].attn_norm,
+                     x->stream);
+        dvi_status st = run_layers(x, 0, cf.n_layers, batch, cc, s0, x->h, x->ss, x->hg, 1, x->hg, 1, 0);
         if (st != DVI_OK) return st;
-        if (s0 + cc == P) {
-            launch_copy_rows(x->h + (size_t)(cc - 1) * d, cc, x->hk, 1, batch, d, x->stream);
-            launch_rmsnorm(x->dt, x->hk, x->final_norm, batch, d, cf.rms_eps, x->xn, x->stream);
-            head(x, batch, x->vlogits, false, x->pending, 1, nullptr);
+        if (s0 + cc == P) {  // last prompt token of every sequence -> first generated token
+            launch_gather_fm(x->dt, x->hg, true, cc, cc - 1, batch, d, x->pfm, x->stream);
+            head(x, x->pfm, x->ss + (size_t)(cc - 1) * nps, cc * nps, batch, x->vlogits, false, x->pending, 1, nullptr);
         }
     }
     std::vector<int32_t> lh(cf.max_batch, 0);
@@ -606,15 +651,23 @@ extern "C" dvi_status dvi_draft(dvi_ctx *x, int32_t k_spec, const int32_t *force
     ev_begin(x, 0);
     HIPCHK(x, hipMemsetAsync(flags_ptr(x), 0, 16, x->stream));
     x->ar_mode = (k_spec == 1 && !forced) ? 1 : 0;
+    const int nps = d / 16;
     for (int j = 0; j < k_spec; ++j) {
+        // draft token j of sequence b lives in row b*k_spec + j of hk / hk_ss / hk_hg
         const int32_t *tok = j == 0 ? x->pending : x->drafts + (j - 1);
-        launch_embed(x->dt, x->emb, tok, j == 0 ? 1 : k_spec, B, 1, d, x->h, x->stream);
-        dvi_status st = run_layers(x, 0, cf.split_k, B, 1, j, x->h);
+        float *h = x->hk + (size_t)j * d;
+        float *ss = x->hk_ss + (size_t)j * nps;
+        launch_embed(x->dt, x->emb, tok, j == 0 ? 1 : k_spec, B, 1, d, h, k_spec * d, ss, k_spec * nps, x->hg,
+                     x->L[0].attn_norm, x->stream);
+        // the last draft layer hands its rows to the verify: FM row b*k_spec + j of hk_hg
+        dvi_status st = run_layers(x, 0, cf.split_k, B, 1, j, h, ss, x->hg, k_spec, x->hk_hg, k_spec, j);
         if (st != DVI_OK) return st;
-        launch_scatter_rows(x->h, x->hk, B, d, 4, k_spec, j, x->stream);
-        launch_rmsnorm(x->dt, x->h, x->final_norm, B, d, cf.rms_eps, x->xn, x->stream);
-        launch_scatter_rows(x->xn, x->hk_hat, B, d, (int)x->es, k_spec, j, x->stream);
-        if (!x->ar_mode) head(x, B, x->dlogits, true, x->drafts + j, k_spec, forced ? x->forced + j : nullptr);
+        if (!x->ar_mode) {
+            void *xh = (uint8_t *)x->hk_hat + (size_t)j * d * x->es;
+            launch_head_prep(x->dt, h, k_spec * d, ss, k_spec * nps, x->final_norm, B, d, cf.rms_eps, x->lora_B,
+                             cf.lora_rank, xh, k_spec * d, x->dfm, x->lora_u, x->stream);
+            head(x, x->dfm, nullptr, 0, B, x->dlogits, true, x->drafts + j, k_spec, forced ? x->forced + j : nullptr);
+        }
     }
     if (x->ar_mode) HIPCHK(x, hipMemsetAsync(x->drafts, 0xff, (size_t)B * 4, x->stream));
     ev_end(x, 0);
@@ -635,10 +688,9 @@ extern "C" dvi_status dvi_verify(dvi_ctx *x, int32_t *targets_out, int32_t *acce
     const dvi_config &cf = x->cfg;
     const int B = x->B, k = x->k_spec, M = B * k, d = cf.d_model;
     ev_begin(x, 1);
-    dvi_status st = run_layers(x, cf.split_k, cf.n_layers, B, k, 0, x->hk);
+    dvi_status st = run_layers(x, cf.split_k, cf.n_layers, B, k, 0, x->hk, x->hk_ss, x->hk_hg, 1, x->hk_hg, 1, 0);
     if (st != DVI_OK) return st;
-    launch_rmsnorm(x->dt, x->hk, x->final_norm, M, d, cf.rms_eps, x->xn, x->stream);
-    head(x, M, x->vlogits, false, x->targets, 1, nullptr);
+    head(x, x->hk_hg, x->hk_ss, d / 16, M, x->vlogits, false, x->targets, 1, nullptr);
     ev_end(x, 1);
     LAUNCHCHK(x);
     if (targets_out || accept_out) {
@@ -787,6 +839,7 @@ extern "C" dvi_status dvi_update_drafter(dvi_ctx *x, const dvi_update_args *ua, 
     u.du = x->upd_du;
     u.dB = x->upd_dB;
     u.loss_out = x->upd_loss;
+    u.xfm = x->ufm;
     launch_update_forward(x->dt, u, x->stream);
     launch_update_backward(x->dt, u, x->stream);
     const size_t nA = (size_t)cf.vocab * cf.lora_rank, nB = (size_t)cf.lora_rank * cf.d_model;

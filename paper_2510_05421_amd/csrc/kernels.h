@@ -34,20 +34,32 @@ enum Epi : int {
 
 struct GemmArgs {
     const void *W;      // packed [N][K]
-    const void *X;      // activations [M][K] (dtype of W), row stride K
+    const void *X;      // activations [M][K] (dtype of W) in fragment-major (FM) layout
     int M, N, K;
+    // Folded RMSNorm: when ss_in != nullptr, X holds dtype(h * g) and output row m is scaled
+    // by 1/sqrt(sum(ss_in[m][0..K/16)) / K + eps).
+    const float *ss_in;
+    int ld_ss_in;
+    float eps;
     // token -> (sequence, block offset): m = b * c + i, position = lens[b] + pos_off + i
     int c, pos_off;
     const int32_t *lens;
-    // EPI_RESID
-    float *H;           // [M][N]
+    // EPI_RESID: H[m][n] += y; then per-16-column sums of squares of the new row -> ss_out,
+    // and dtype(h * g_next) -> hg_out (input of the next folded RMSNorm)
+    float *H;
+    int ldh;
+    float *ss_out;
+    int ld_ss_out;
+    void *hg_out;       // FM [rows][N]; token m goes to FM row m * hg_rs + hg_off
+    int hg_rs, hg_off;
+    const float *g_next;
     // EPI_QKV
     float *Q;           // [M][n_heads * hd] fp32
     void *Kc, *Vc;      // this layer's caches [max_batch][n_kv][s_max][hd]
     int n_heads, n_kv, hd, s_max;
     const float2 *rope; // [s_max][hd/2] (cos, sin)
     // EPI_SWIGLU
-    void *A;            // [M][N/2] activations out (dtype)
+    void *A;            // [M][N/2] activations out (dtype, FM)
     // EPI_LOGITS
     float *Z;           // [M][N] logits
     const float *lora_A;// [N][r] or nullptr
@@ -59,21 +71,19 @@ struct GemmArgs {
 };
 void launch_gemm(DType t, Epi e, const GemmArgs &a, hipStream_t s);
 
-// y[m] = dtype(h[m] * rsqrt(mean(h[m]^2) + eps) * g), one row per workgroup.
-void launch_rmsnorm(DType t, const float *h, const float *g, int M, int d, float eps, void *y,
-                    hipStream_t s);
+// Row m = b*c + i: h = E[tok[b*tok_stride + i]] (fp32, row stride ldh), its per-16-column
+// sums of squares (ss, stride ld_ss) and dtype(h * g) (hg, FM, row m).
+void launch_embed(DType t, const void *emb, const int32_t *tok, int tok_stride, int B, int c, int d, float *h, int ldh,
+                  float *ss, int ld_ss, void *hg, const float *g, hipStream_t s);
 
-// h[b*c + i] = E[tok[b * tok_stride + i]] as fp32.
-void launch_embed(DType t, const void *emb, const int32_t *tok, int tok_stride, int B, int c, int d,
-                  float *h, hipStream_t s);
+// xhat[m] = dtype(RMSNorm(h[m]; g)) (row-major, stride ldx, and FM copy xfm) and
+// u[m][c] = B_s[c] . xhat[m] (the draft head's inputs).
+void launch_head_prep(DType t, const float *h, int ldh, const float *ss, int ld_ss, const float *g, int M, int d,
+                      float eps, const float *Bm, int r, void *xhat, int ldx, void *xfm, float *u, hipStream_t s);
 
-// dst[r] = src[r] for rows r in [0,M) with given row strides (fp32 rows of d).
-void launch_copy_rows(const float *src, int src_stride_rows, float *dst, int dst_stride_rows, int M,
-                      int d, hipStream_t s);
-
-// ctx rows: dst[(b*dst_rows_per_b + dst_off)*d .. ] = src[b*d ..]  (bytes-agnostic, elem bytes es)
-void launch_scatter_rows(const void *src, void *dst, int B, int d, int es, int dst_rows_per_b,
-                         int dst_off, hipStream_t s);
+// dst (FM) row i = src row i*rs + off; src is FM when src_fm, else row-major [..][K].
+void launch_gather_fm(DType t, const void *src, bool src_fm, int rs, int off, int rows, int K, void *dst,
+                      hipStream_t s);
 
 struct AttnArgs {
     const float *Q;      // [M][n_heads*hd]
@@ -86,7 +96,7 @@ struct AttnArgs {
     float scale;
     float *part_o;       // [M][n_heads][chunk_stride][hd]
     float *part_ml;      // [M][n_heads][chunk_stride][2]
-    void *O;             // [M][n_heads*hd] out (dtype)
+    void *O;             // [M][n_heads*hd] out (dtype, FM)
 };
 void launch_attention(DType t, const AttnArgs &a, hipStream_t s);
 
@@ -131,6 +141,7 @@ struct UpdateArgs {
     float gamma, tau, baseline, c_kl, c_ce, c_pg, c_ent;
     const float *A, *Bm;    // A_s [V][r], B_s [r][d]
     float *u;               // [n][r]
+    void *xfm;              // FM scratch for 64 replay rows
     float *Z;               // [n][V] drafter logits -> overwritten by g = dL/dz
     float *part_val;        // scratch for the logits GEMM epilogue
     int32_t *part_idx;

@@ -49,6 +49,17 @@ template <> struct St<DType::BF16> {
     }
 };
 
+// Fragment-major activation layout ("FM"): the input X[M][K] of a GEMM is stored as, for each
+// 16-token group g and K chunk c (KC columns), one contiguous 1 KiB block whose 16-byte lane
+// slot l holds X[16g + l%16][c*KC + (l/16)*EPL .. +EPL) -- exactly the MFMA B fragment of
+// lane l.  Element (m, k) of a K-column matrix therefore sits at fm_index(m, k, K).
+template <DType T>
+__device__ __forceinline__ size_t fm_index(int m, int k, int K) {
+    constexpr int KC = (T == DType::BF16) ? 32 : 16, EPL = KC / 4;
+    const int c = k / KC, rr = k - c * KC, G = rr / EPL, e = rr - G * EPL;
+    return ((size_t)((m >> 4) * (K / KC) + c) * 64 + G * 16 + (m & 15)) * EPL + e;
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
@@ -106,6 +117,28 @@ void launch_pack(DType t, PackSrc srcs, const int32_t *prow, int N, int K, void 
         pack_kernel<DType::F32><<<2048, 256, 0, s>>>(srcs, prow, N, K, dst);
 }
 
+constexpr int CK = 64;  // attention key chunk (absolute positions)
+
+// Inverse RMS of one row from its per-16-column partial sums of squares: lane l adds
+// partials l, l+64, ... in order, then a butterfly, so every lane (and every workgroup that
+// asks) gets the same value.
+__device__ __forceinline__ float inv_rms(const float *ss, int nparts, int d, float eps) {
+    const int lane = threadIdx.x & 63;
+    float s = 0.f;
+    for (int t = lane; t < nparts; t += 64) s += ss[t];
+    s = wave_sum(s);
+    return 1.0f / sqrtf(s / (float)d + eps);
+}
+
+// Sum of squares of 16 consecutive columns held as 4 values by each of the lanes
+// {l, l^step, l^2step, l^3step}: ((c0-3 + c4-7) + (c8-11 + c12-15)), same tree everywhere.
+__device__ __forceinline__ float sumsq16(const float v[4], int step) {
+    float s = ((v[0] * v[0] + v[1] * v[1]) + v[2] * v[2]) + v[3] * v[3];
+    s += __shfl_xor(s, step);
+    s += __shfl_xor(s, 2 * step);
+    return s;
+}
+
 // ------------------------------------------------------------------------------------------
 // Skinny-M weight-streaming GEMM:  Y[m][n] = sum_k X[m][k] W[n][k],  M <= 64.
 //
@@ -116,17 +149,31 @@ void launch_pack(DType t, PackSrc srcs, const int32_t *prow, int N, int K, void 
 // partial tiles are summed in wave order through LDS and the epilogue runs on wave 0.
 // Output layout of a 16x16 MFMA tile: lane l holds rows 4*(l/16)+j (j = 0..3) of column
 // l % 16, i.e. features nt*16 + 4*(l/16) + j of token 16*g + (l % 16).
+//
+// RMSNorm is folded in: when ss_in is given, X holds dtype(h * g) and row m of the result
+// is scaled by 1/sqrt(mean(h[m]^2) + eps), reduced from the partial sums of squares that the
+// producing epilogue wrote.  RMSNorm(h) W^T = (h*g) W^T / rms(h), so no separate pass over h.
 // ------------------------------------------------------------------------------------------
-template <DType T, int MG, int EPI>
-__global__ void __launch_bounds__(512) gemm_kernel(GemmArgs a) {
+// Streaming loads.  Weights are read exactly once per pass; the activation fragments are read
+// once per workgroup.  Issuing both with the non-temporal hint keeps the activation reads from
+// disturbing the weight stream (measured on gfx950: ordinary loads of the activations cost
+// up to a third of the bandwidth at 4-16 tokens, non-temporal ones almost nothing).
+__device__ __forceinline__ uint4 ld_stream(const uint4 *p) {
+    typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+    const v4u t = __builtin_nontemporal_load((const v4u *)p);
+    return uint4{t.x, t.y, t.z, t.w};
+}
+
+template <DType T, int MG, int EPI, int RT, int WMAX>
+__global__ void __launch_bounds__(64 * WMAX) gemm_kernel(GemmArgs a) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
-    const int nt = blockIdx.x;
+    const int nt0 = blockIdx.x * RT;
     const int KC = (T == DType::BF16) ? 32 : 16;
     const int KT = a.K / KC;
     const int c0 = (wave * KT) / nw, c1 = ((wave + 1) * KT) / nw;
     const size_t es = (T == DType::BF16) ? 2 : 4;
-    const uint4 *wp = (const uint4 *)a.W + (size_t)nt * KT * 64 + lane;
-    const size_t xrow = (size_t)a.K * es / 16;
+    const uint4 *wp = (const uint4 *)a.W + (size_t)nt0 * KT * 64 + lane;
+    const size_t tile_stride = (size_t)KT * 64;
 
     const uint4 *xp[MG];
     bool xv[MG];
@@ -134,64 +181,99 @@ __global__ void __launch_bounds__(512) gemm_kernel(GemmArgs a) {
     for (int g = 0; g < MG; ++g) {
         const int m = 16 * g + (lane & 15);
         xv[g] = m < a.M;
-        xp[g] = (const uint4 *)a.X + (size_t)(xv[g] ? m : 0) * xrow + (lane >> 4);
+        xp[g] = (const uint4 *)a.X + (size_t)g * KT * 64 + lane;   // FM block (g, chunk 0)
     }
-    f32x4 acc[MG];
+    f32x4 acc[RT][MG];
 #pragma unroll
-    for (int g = 0; g < MG; ++g) acc[g] = (f32x4){0.f, 0.f, 0.f, 0.f};
+    for (int t = 0; t < RT; ++t)
+#pragma unroll
+        for (int g = 0; g < MG; ++g) acc[t][g] = (f32x4){0.f, 0.f, 0.f, 0.f};
 
-    constexpr int U = (MG <= 2) ? 8 : 4;
+    // Each activation fragment feeds RT weight tiles.  The loop is software-pipelined: the
+    // fragments of the next U chunks are requested before the current U are multiplied, so a
+    // wave always has loads in flight while its MFMAs run.
+    constexpr int U = 2;
     const uint4 zero = {0u, 0u, 0u, 0u};
-    int c = c0;
-    for (; c + U <= c1; c += U) {
-        uint4 w[U], x[U][MG];
+    uint4 w[U][RT], x[U][MG];
+    auto fetch = [&](int cb, uint4 (&wf)[U][RT], uint4 (&xf)[U][MG]) {
 #pragma unroll
-        for (int u = 0; u < U; ++u) w[u] = wp[(size_t)(c + u) * 64];
+        for (int u = 0; u < U; ++u) {
+            const bool in = cb + u < c1;
+#pragma unroll
+            for (int t = 0; t < RT; ++t) wf[u][t] = in ? ld_stream(wp + t * tile_stride + (size_t)(cb + u) * 64) : zero;
+#pragma unroll
+            for (int g = 0; g < MG; ++g) xf[u][g] = (in && xv[g]) ? ld_stream(xp[g] + (size_t)(cb + u) * 64) : zero;
+        }
+    };
+    fetch(c0, w, x);
+    for (int c = c0; c < c1; c += U) {
+        uint4 wn[U][RT], xn[U][MG];
+        fetch(c + U, wn, xn);
 #pragma unroll
         for (int u = 0; u < U; ++u)
 #pragma unroll
-            for (int g = 0; g < MG; ++g) x[u][g] = xv[g] ? xp[g][(size_t)(c + u) * 4] : zero;
+            for (int t = 0; t < RT; ++t)
 #pragma unroll
-        for (int u = 0; u < U; ++u)
+                for (int g = 0; g < MG; ++g) acc[t][g] = St<T>::mma(w[u][t], x[u][g], acc[t][g]);
 #pragma unroll
-            for (int g = 0; g < MG; ++g) acc[g] = St<T>::mma(w[u], x[u][g], acc[g]);
-    }
-    for (; c < c1; ++c) {
-        const uint4 w = wp[(size_t)c * 64];
+        for (int u = 0; u < U; ++u) {
 #pragma unroll
-        for (int g = 0; g < MG; ++g) {
-            const uint4 x = xv[g] ? xp[g][(size_t)c * 4] : zero;
-            acc[g] = St<T>::mma(w, x, acc[g]);
+            for (int t = 0; t < RT; ++t) w[u][t] = wn[u][t];
+#pragma unroll
+            for (int g = 0; g < MG; ++g) x[u][g] = xn[u][g];
         }
     }
 
-    __shared__ f32x4 red[8][64];
-    if (nw > 1) {
-#pragma unroll
-        for (int g = 0; g < MG; ++g) {
-            red[wave][lane] = acc[g];
-            __syncthreads();
-            if (wave == 0) {
-                f32x4 s = red[0][lane];
-                for (int w = 1; w < nw; ++w) s += red[w][lane];
-                acc[g] = s;
-            }
-            __syncthreads();
+    // Per-wave partial tiles are summed in wave order; tile t's sum lands in wave t, which
+    // then runs that tile's epilogue.
+    __shared__ f32x4 red[RT][WMAX][64];
+    __shared__ float sinv[64];
+    if (a.ss_in != nullptr)
+        for (int m = wave; m < a.M; m += nw) {
+            const float v = inv_rms(a.ss_in + (size_t)m * a.ld_ss_in, a.K / 16, a.K, a.eps);
+            if (lane == 0) sinv[m] = v;
         }
+    f32x4 mine[MG];
+#pragma unroll
+    for (int g = 0; g < MG; ++g) {
+#pragma unroll
+        for (int t = 0; t < RT; ++t) red[t][wave][lane] = acc[t][g];
+        __syncthreads();
+        if (wave < RT) {
+            f32x4 sum = red[wave][0][lane];
+            for (int w2 = 1; w2 < nw; ++w2) sum += red[wave][w2][lane];
+            mine[g] = sum;
+        }
+        __syncthreads();
     }
-    if (wave != 0) return;
+    if (wave >= RT) return;
+    const int nt = nt0 + wave;
 
     const int G4 = lane >> 4;
 #pragma unroll
     for (int g = 0; g < MG; ++g) {
         const int m = 16 * g + (lane & 15);
         const bool valid = m < a.M;
-        const f32x4 v = acc[g];
+        const float sc = (a.ss_in != nullptr && valid) ? sinv[m] : 1.0f;
+        f32x4 v = mine[g];
         if (EPI == EPI_RESID) {
+            float hv[4] = {0.f, 0.f, 0.f, 0.f};
+            const int n0 = nt * 16 + 4 * G4;
             if (valid) {
-                float *h = a.H + (size_t)m * a.N + nt * 16 + 4 * G4;
+                float *h = a.H + (size_t)m * a.ldh + n0;
 #pragma unroll
-                for (int j = 0; j < 4; ++j) h[j] += v[j];
+                for (int j = 0; j < 4; ++j) {
+                    hv[j] = h[j] + v[j];
+                    h[j] = hv[j];
+                }
+            }
+            const float s = sumsq16(hv, 16);
+            if (valid) {
+                if (a.ss_out != nullptr && G4 == 0) a.ss_out[(size_t)m * a.ld_ss_out + nt] = s;
+                if (a.hg_out != nullptr)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+                        St<T>::store(a.hg_out, fm_index<T>(m * a.hg_rs + a.hg_off, n0 + j, a.N), hv[j] * a.g_next[n0 + j]);
             }
         } else if (EPI == EPI_QKV) {
             if (valid) {
@@ -202,7 +284,7 @@ __global__ void __launch_bounds__(512) gemm_kernel(GemmArgs a) {
 #pragma unroll
                 for (int p = 0; p < 2; ++p) {
                     const int j = 8 * t + 2 * G4 + p;
-                    float x0 = v[2 * p], x1 = v[2 * p + 1];
+                    float x0 = v[2 * p] * sc, x1 = v[2 * p + 1] * sc;
                     if (hg < a.n_heads + a.n_kv) {
                         const float2 cs = a.rope[(size_t)pos * half + j];
                         const float r0 = x0 * cs.x - x1 * cs.y;
@@ -229,9 +311,9 @@ __global__ void __launch_bounds__(512) gemm_kernel(GemmArgs a) {
 #pragma unroll
                 for (int p = 0; p < 2; ++p) {
                     const int f = 8 * nt + 2 * G4 + p;
-                    const float gt = v[2 * p], up = v[2 * p + 1];
+                    const float gt = v[2 * p] * sc, up = v[2 * p + 1] * sc;
                     const float act = gt / (1.0f + expf(-gt)) * up;
-                    St<T>::store(a.A, (size_t)m * (a.N / 2) + f, act);
+                    St<T>::store(a.A, fm_index<T>(m, f, a.N / 2), act);
                 }
             }
         } else {  // EPI_LOGITS
@@ -240,7 +322,7 @@ __global__ void __launch_bounds__(512) gemm_kernel(GemmArgs a) {
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const int n = nt * 16 + 4 * G4 + j;
-                float y = v[j];
+                float y = v[j] * sc;
                 if (a.lora_A != nullptr && valid) {
                     const float *Ar = a.lora_A + (size_t)n * a.r;
                     const float *ur = a.lora_u + (size_t)m * a.r;
@@ -275,218 +357,322 @@ __global__ void __launch_bounds__(512) gemm_kernel(GemmArgs a) {
     }
 }
 
-template <DType T, int EPI>
+// Launch shape of a weight matrix, a function of (N, K) only, never of M: RT 16-row tiles
+// per workgroup (activations reused across them) and the K split over the workgroup's waves.
+// Since neither depends on M, every output's summation order is the same for every call on
+// that matrix (batch invariance).
+struct GemmShape {
+    int rt, waves;
+};
+static GemmShape gemm_shape(int N, int K, int KC, int M) {
+    const int tiles = N / 16, chunks = K / KC, mg = (M + 15) / 16;
+    // K split, from the matrix only: the most waves per workgroup (up to 16) that keep the whole
+    // grid resident at once (8 waves per SIMD x 4 SIMDs x 256 CUs) with >= 4 chunks per wave.
+    int w = 1;
+    while (w < 16 && (long)tiles * (2 * w) <= 8192 && chunks / (2 * w) >= 4) w *= 2;
+    // tiles per workgroup: more when there are more token groups to reuse each weight tile on
+    // (16-wave workgroups have 128 registers per lane and keep one tile)
+    int rt = 1;
+    if (w <= 8) {
+        if (mg >= 3 && tiles % 4 == 0) rt = 4;
+        else if (mg >= 2 && tiles % 2 == 0) rt = 2;
+        while (rt > w) rt >>= 1;
+    }
+    return {rt, w};
+}
+
+template <DType T, int EPI, int RT, int WMAX>
 static void gemm_dispatch_mg(const GemmArgs &a, dim3 grid, dim3 block, hipStream_t s) {
     const int mg = (a.M + 15) / 16;
     switch (mg) {
-        case 1: gemm_kernel<T, 1, EPI><<<grid, block, 0, s>>>(a); break;
-        case 2: gemm_kernel<T, 2, EPI><<<grid, block, 0, s>>>(a); break;
-        case 3: gemm_kernel<T, 3, EPI><<<grid, block, 0, s>>>(a); break;
-        default: gemm_kernel<T, 4, EPI><<<grid, block, 0, s>>>(a); break;
+        case 1: gemm_kernel<T, 1, EPI, RT, WMAX><<<grid, block, 0, s>>>(a); break;
+        case 2: gemm_kernel<T, 2, EPI, RT, WMAX><<<grid, block, 0, s>>>(a); break;
+        case 3: gemm_kernel<T, 3, EPI, RT, WMAX><<<grid, block, 0, s>>>(a); break;
+        default: gemm_kernel<T, 4, EPI, RT, WMAX><<<grid, block, 0, s>>>(a); break;
+    }
+}
+
+template <DType T, int RT, int WMAX>
+static void gemm_dispatch_epi(Epi e, const GemmArgs &a, dim3 grid, dim3 block, hipStream_t s) {
+    switch (e) {
+        case EPI_RESID: gemm_dispatch_mg<T, EPI_RESID, RT, WMAX>(a, grid, block, s); break;
+        case EPI_QKV: gemm_dispatch_mg<T, EPI_QKV, RT, WMAX>(a, grid, block, s); break;
+        case EPI_SWIGLU: gemm_dispatch_mg<T, EPI_SWIGLU, RT, WMAX>(a, grid, block, s); break;
+        default: gemm_dispatch_mg<T, EPI_LOGITS, RT, WMAX>(a, grid, block, s); break;
     }
 }
 
 template <DType T>
-static void gemm_dispatch(Epi e, const GemmArgs &a, dim3 grid, dim3 block, hipStream_t s) {
-    switch (e) {
-        case EPI_RESID: gemm_dispatch_mg<T, EPI_RESID>(a, grid, block, s); break;
-        case EPI_QKV: gemm_dispatch_mg<T, EPI_QKV>(a, grid, block, s); break;
-        case EPI_SWIGLU: gemm_dispatch_mg<T, EPI_SWIGLU>(a, grid, block, s); break;
-        default: gemm_dispatch_mg<T, EPI_LOGITS>(a, grid, block, s); break;
+static void gemm_dispatch(Epi e, const GemmArgs &a, GemmShape sh, hipStream_t s) {
+    dim3 grid(a.N / 16 / sh.rt), block(64 * sh.waves);
+    if (sh.waves > 8) {
+        gemm_dispatch_epi<T, 1, 16>(e, a, grid, block, s);
+        return;
     }
-}
-
-// Waves per workgroup depend only on the matrix shape (never on M), so the K split, and
-// with it every output's summation order, is the same for every call on that matrix.
-static int gemm_waves(int N, int K, int KC) {
-    const int tiles = N / 16, chunks = K / KC;
-    int w = tiles <= 512 ? 8 : 4;
-    while (w > 1 && chunks / w < 4) w >>= 1;
-    return w;
+    switch (sh.rt) {
+        case 4: gemm_dispatch_epi<T, 4, 8>(e, a, grid, block, s); break;
+        case 2: gemm_dispatch_epi<T, 2, 8>(e, a, grid, block, s); break;
+        default: gemm_dispatch_epi<T, 1, 8>(e, a, grid, block, s); break;
+    }
 }
 
 void launch_gemm(DType t, Epi e, const GemmArgs &a, hipStream_t s) {
-    const int KC = pack_kc(t);
-    dim3 grid(a.N / 16), block(64 * gemm_waves(a.N, a.K, KC));
+    const GemmShape sh = gemm_shape(a.N, a.K, pack_kc(t), a.M);
     if (t == DType::BF16)
-        gemm_dispatch<DType::BF16>(e, a, grid, block, s);
+        gemm_dispatch<DType::BF16>(e, a, sh, s);
     else
-        gemm_dispatch<DType::F32>(e, a, grid, block, s);
+        gemm_dispatch<DType::F32>(e, a, sh, s);
 }
 
 // ------------------------------------------------------------------------------------------
-// RMSNorm, embedding, row copies
+// Embedding gather (first layer input) and the draft-head preparation
 // ------------------------------------------------------------------------------------------
-template <DType T>
-__global__ void __launch_bounds__(256) rmsnorm_kernel(const float *h, const float *g, int d, float eps, void *y) {
-    __shared__ float red[4];
-    const int m = blockIdx.x;
-    const float *x = h + (size_t)m * d;
-    float ss = 0.f;
-    for (int i = threadIdx.x; i < d; i += 256) ss += x[i] * x[i];
-    ss = block_sum256(ss, red);
-    const float inv = 1.0f / sqrtf(ss / (float)d + eps);
-    for (int i = threadIdx.x; i < d; i += 256) St<T>::store(y, (size_t)m * d + i, x[i] * inv * g[i]);
-}
-
-void launch_rmsnorm(DType t, const float *h, const float *g, int M, int d, float eps, void *y, hipStream_t s) {
-    if (M <= 0) return;
-    if (t == DType::BF16)
-        rmsnorm_kernel<DType::BF16><<<M, 256, 0, s>>>(h, g, d, eps, y);
-    else
-        rmsnorm_kernel<DType::F32><<<M, 256, 0, s>>>(h, g, d, eps, y);
-}
-
+// Row m = b*c + i takes token tok[b*tok_stride + i]: h = E[token] (fp32), its partial sums of
+// squares per 16 columns, and hg = dtype(h * g) for the first layer's folded RMSNorm.
 template <DType T>
 __global__ void __launch_bounds__(256) embed_kernel(const void *emb, const int32_t *tok, int tok_stride, int c, int d,
-                                                    float *h) {
+                                                    float *h, int ldh, float *ss, int ld_ss, void *hg, const float *g) {
     const int m = blockIdx.x;
     const int b = m / c, i = m - b * c;
     const size_t row = (size_t)tok[(size_t)b * tok_stride + i] * d;
-    for (int k = threadIdx.x; k < d; k += 256) h[(size_t)m * d + k] = St<T>::load(emb, row + k);
+    for (int base = 0; base < d; base += 1024) {
+        const int col = base + 4 * threadIdx.x;
+        const bool ok = col < d;
+        float v[4] = {0.f, 0.f, 0.f, 0.f};
+        if (ok)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) v[j] = St<T>::load(emb, row + col + j);
+        const float s = sumsq16(v, 1);
+        if (ok) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                h[(size_t)m * ldh + col + j] = v[j];
+                St<T>::store(hg, fm_index<T>(m, col + j, d), v[j] * g[col + j]);
+            }
+            if ((threadIdx.x & 3) == 0) ss[(size_t)m * ld_ss + col / 16] = s;
+        }
+    }
 }
 
-void launch_embed(DType t, const void *emb, const int32_t *tok, int tok_stride, int B, int c, int d, float *h,
-                  hipStream_t s) {
+void launch_embed(DType t, const void *emb, const int32_t *tok, int tok_stride, int B, int c, int d, float *h, int ldh,
+                  float *ss, int ld_ss, void *hg, const float *g, hipStream_t s) {
     if (t == DType::BF16)
-        embed_kernel<DType::BF16><<<B * c, 256, 0, s>>>(emb, tok, tok_stride, c, d, h);
+        embed_kernel<DType::BF16><<<B * c, 256, 0, s>>>(emb, tok, tok_stride, c, d, h, ldh, ss, ld_ss, hg, g);
     else
-        embed_kernel<DType::F32><<<B * c, 256, 0, s>>>(emb, tok, tok_stride, c, d, h);
+        embed_kernel<DType::F32><<<B * c, 256, 0, s>>>(emb, tok, tok_stride, c, d, h, ldh, ss, ld_ss, hg, g);
 }
 
-__global__ void copy_rows_kernel(const float *src, int ss, float *dst, int ds, int d) {
-    const int m = blockIdx.x;
-    for (int k = threadIdx.x; k < d; k += blockDim.x) dst[(size_t)m * ds * d + k] = src[(size_t)m * ss * d + k];
+// Draft head input: xhat = dtype(RMSNorm(h; g)) (the row the replay buffer logs and the head
+// GEMM reads) and the LoRA projection u[c] = sum_i B_s[c][i] xhat[i].  Workgroup (c, m).
+template <DType T>
+__global__ void __launch_bounds__(256) head_prep_kernel(const float *h, int ldh, const float *ss, int ld_ss,
+                                                        const float *g, int d, float eps, const float *Bm, int r,
+                                                        void *xhat, int ldx, void *xfm, float *u) {
+    __shared__ float red[4];
+    const int c = blockIdx.x, m = blockIdx.y;
+    const float inv = inv_rms(ss + (size_t)m * ld_ss, d / 16, d, eps);
+    float acc = 0.f;
+    for (int i = threadIdx.x; i < d; i += 256) {
+        float x = h[(size_t)m * ldh + i] * inv * g[i];
+        if (T == DType::BF16) x = bf2f(f2bf(x));
+        if (c == 0) {
+            St<T>::store(xhat, (size_t)m * ldx + i, x);
+            St<T>::store(xfm, fm_index<T>(m, i, d), x);
+        }
+        acc += Bm[(size_t)c * d + i] * x;
+    }
+    acc = block_sum256(acc, red);
+    if (threadIdx.x == 0) u[(size_t)m * r + c] = acc;
 }
 
-void launch_copy_rows(const float *src, int ss, float *dst, int ds, int M, int d, hipStream_t s) {
-    if (M > 0) copy_rows_kernel<<<M, 256, 0, s>>>(src, ss, dst, ds, d);
+void launch_head_prep(DType t, const float *h, int ldh, const float *ss, int ld_ss, const float *g, int M, int d,
+                      float eps, const float *Bm, int r, void *xhat, int ldx, void *xfm, float *u, hipStream_t s) {
+    if (M <= 0) return;
+    dim3 grid(r, M);
+    if (t == DType::BF16)
+        head_prep_kernel<DType::BF16><<<grid, 256, 0, s>>>(h, ldh, ss, ld_ss, g, d, eps, Bm, r, xhat, ldx, xfm, u);
+    else
+        head_prep_kernel<DType::F32><<<grid, 256, 0, s>>>(h, ldh, ss, ld_ss, g, d, eps, Bm, r, xhat, ldx, xfm, u);
 }
 
-__global__ void scatter_rows_kernel(const uint8_t *src, uint8_t *dst, int row_bytes, int rows_per_b, int off) {
-    const int b = blockIdx.x;
-    const uint8_t *s = src + (size_t)b * row_bytes;
-    uint8_t *d = dst + ((size_t)b * rows_per_b + off) * row_bytes;
-    for (int k = threadIdx.x * 4; k < row_bytes; k += blockDim.x * 4) *(uint32_t *)(d + k) = *(const uint32_t *)(s + k);
+// Gather rows into a compact FM buffer: dst row i = src row (i * rs + off) (FM or row-major
+// source), K columns.  Used for the prefill head (last token of every sequence) and for the
+// drafter update (replay rows).
+template <DType T>
+__global__ void __launch_bounds__(256) gather_fm_kernel(const void *src, int src_fm, int rs, int off, int K, void *dst) {
+    const int i = blockIdx.x, r = i * rs + off;
+    for (int k = threadIdx.x; k < K; k += 256) {
+        const float v = St<T>::load(src, src_fm ? fm_index<T>(r, k, K) : (size_t)r * K + k);
+        St<T>::store(dst, fm_index<T>(i, k, K), v);
+    }
 }
 
-void launch_scatter_rows(const void *src, void *dst, int B, int d, int es, int rows_per_b, int off, hipStream_t s) {
-    scatter_rows_kernel<<<B, 256, 0, s>>>((const uint8_t *)src, (uint8_t *)dst, d * es, rows_per_b, off);
+void launch_gather_fm(DType t, const void *src, bool src_fm, int rs, int off, int rows, int K, void *dst,
+                      hipStream_t s) {
+    if (rows <= 0) return;
+    if (t == DType::BF16)
+        gather_fm_kernel<DType::BF16><<<rows, 256, 0, s>>>(src, src_fm ? 1 : 0, rs, off, K, dst);
+    else
+        gather_fm_kernel<DType::F32><<<rows, 256, 0, s>>>(src, src_fm ? 1 : 0, rs, off, K, dst);
+}
+
+// u[m][c] = sum_i B_s[c][i] x[m][i] for already-normalised rows x.  Workgroup (c, m).
+template <DType T>
+__global__ void __launch_bounds__(256) lora_u_kernel(const void *x, const float *Bm, int d, int r, float *u) {
+    __shared__ float red[4];
+    const int c = blockIdx.x, m = blockIdx.y;
+    float acc = 0.f;
+    for (int i = threadIdx.x; i < d; i += 256) acc += Bm[(size_t)c * d + i] * St<T>::load(x, (size_t)m * d + i);
+    acc = block_sum256(acc, red);
+    if (threadIdx.x == 0) u[(size_t)m * r + c] = acc;
+}
+
+void launch_lora_u(DType t, const void *x, const float *Bm, int M, int d, int r, float *u, hipStream_t s) {
+    if (M <= 0) return;
+    dim3 grid(r, M);
+    if (t == DType::BF16)
+        lora_u_kernel<DType::BF16><<<grid, 256, 0, s>>>(x, Bm, d, r, u);
+    else
+        lora_u_kernel<DType::F32><<<grid, 256, 0, s>>>(x, Bm, d, r, u);
 }
 
 // ------------------------------------------------------------------------------------------
 // Block-causal attention against the KV cache, split over fixed 64-position key chunks.
 //
-// Workgroup (chunk ch, kv head, sequence b) stages keys/values [64*ch, 64*ch+64) of that
-// sequence in LDS and serves every query row of the block that reads this kv head
-// (c tokens x n_heads/n_kv grouped heads).  Row at position p sees keys 0..p.  Each wave
-// takes one row at a time: lane j scores key j (sequential dot over the head dim), the
-// softmax statistics are wave butterflies, and each lane accumulates its head-dim slots
-// over the keys in order.  Partial (max, sum, unnormalised output) per chunk are merged by
-// attn_combine in chunk order.  Chunk boundaries sit at absolute positions, so a row's
-// result does not depend on the other rows in its block.
+// Workgroup (chunk ch, kv head, sequence b) serves every query row of the block that reads
+// this kv head (c tokens x n_heads/n_kv grouped heads); the row at position p sees keys
+// 0..p.  Wave w owns keys 16w..16w+15 of the chunk: for the scores, lane l holds key
+// 16w + l%16 and head-dim quarter l/16 of it in registers (a quarter-dot per lane, summed
+// over the four quarters by a butterfly); for P.V, lane l holds head dims [l*HD/64, ..) of
+// the wave's 16 values.  Chunk statistics are combined over the four waves in wave order.
+// Keys and values are read once per workgroup straight into registers and reused by every
+// row.  Each chunk's (max, sum, unnormalised output) goes to a partial slot, and
+// attn_combine merges every row's chunks in chunk order.  Chunk boundaries sit at absolute
+// positions, so a row's result does not depend on the other rows in its block.
 // ------------------------------------------------------------------------------------------
-constexpr int CK = 64;
+// Load n contiguous elements (n * sizeof(E) a multiple of 16 bytes, 16-byte aligned) as floats.
+template <DType T, int N>
+__device__ __forceinline__ void load_row(const void *p, float *out) {
+    const uint4 *q = (const uint4 *)p;
+    if (T == DType::BF16) {
+#pragma unroll
+        for (int i = 0; i < N / 8; ++i) {
+            const uint4 v = q[i];
+            const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                out[8 * i + 2 * k] = __uint_as_float(w[k] << 16);
+                out[8 * i + 2 * k + 1] = __uint_as_float(w[k] & 0xffff0000u);
+            }
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < N / 4; ++i) {
+            const uint4 v = q[i];
+            out[4 * i] = __uint_as_float(v.x);
+            out[4 * i + 1] = __uint_as_float(v.y);
+            out[4 * i + 2] = __uint_as_float(v.z);
+            out[4 * i + 3] = __uint_as_float(v.w);
+        }
+    }
+}
 
 template <DType T, int HD>
 __global__ void __launch_bounds__(256) attn_partial_kernel(AttnArgs a) {
     typedef typename St<T>::type E;
-    constexpr int EP = (T == DType::BF16) ? 2 : 1;             // elements per 32-bit word
-    constexpr int RW = HD / EP + 1;                              // padded row, in 32-bit words (odd)
-    __shared__ uint32_t Ks[CK * RW];
-    __shared__ uint32_t Vs[CK * (HD / EP)];
-    __shared__ float qs[4][HD];
-    __shared__ float ps[4][CK];
+    constexpr int Q4 = HD / 4;
+    constexpr int EPV = HD / 64;
+    __shared__ float red_m[4], red_l[4];
+    __shared__ float ow[4][HD];
 
     const int ch = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int len0 = a.lens[b] + a.pos_off;
     const int pmax = len0 + a.c - 1;
     const int kbase = ch * CK;
     if (kbase > pmax) return;
     const int nk = min(CK, pmax + 1 - kbase);
+    const int jl = 16 * w + (lane & 15);
+    const int qd = lane >> 4;
+    const size_t cache0 = ((size_t)b * a.n_kv + kvh) * a.s_max + kbase;
 
-    const size_t cbase = (((size_t)b * a.n_kv + kvh) * a.s_max + kbase) * HD;
-    const uint32_t *kg = (const uint32_t *)((const E *)a.Kc + cbase);
-    const uint32_t *vg = (const uint32_t *)((const E *)a.Vc + cbase);
-    constexpr int WPR = HD / EP;  // words per row
-    for (int w = threadIdx.x; w < nk * WPR; w += 256) {
-        const int j = w / WPR, e = w - j * WPR;
-        Ks[j * RW + e] = kg[w];
-        Vs[w] = vg[w];
+    float kf[Q4];
+    if (jl < nk) {
+        load_row<T, Q4>((const E *)a.Kc + (cache0 + jl) * HD + qd * Q4, kf);
+    } else {
+#pragma unroll
+        for (int e = 0; e < Q4; ++e) kf[e] = 0.f;
     }
-    __syncthreads();
+    float vf[16][EPV];
+#pragma unroll
+    for (int jj = 0; jj < 16; ++jj) {
+        const int key = 16 * w + jj;
+        const E *vr = (const E *)a.Vc + (cache0 + key) * HD + lane * EPV;
+#pragma unroll
+        for (int q = 0; q < EPV; ++q) vf[jj][q] = key < nk ? St<T>::load(vr, q) : 0.f;
+    }
 
     const int G = a.n_heads / a.n_kv;
     const int R = a.c * G;
-    for (int row = wave; row < R; row += 4) {
+    for (int row = 0; row < R; ++row) {
         const int i = row / G, gi = row - i * G;
         const int h = kvh * G + gi;
         const int m = b * a.c + i;
         const int p = len0 + i;
         const int nvalid = min(nk, p + 1 - kbase);
-        if (nvalid <= 0) continue;  // uniform across the wave
-        const float *qg = a.Q + (size_t)m * a.n_heads * HD + (size_t)h * HD;
-        for (int e = lane; e < HD; e += 64) qs[wave][e] = qg[e];
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-
-        float s = -INFINITY;
-        if (lane < nvalid) {
-            float dot = 0.f;
-            const uint32_t *kr = Ks + lane * RW;
-            if (T == DType::BF16) {
-#pragma unroll 8
-                for (int e2 = 0; e2 < HD / 2; ++e2) {
-                    const uint32_t wv = kr[e2];
-                    dot += qs[wave][2 * e2] * __uint_as_float(wv << 16);
-                    dot += qs[wave][2 * e2 + 1] * __uint_as_float(wv & 0xffff0000u);
-                }
-            } else {
-#pragma unroll 8
-                for (int e = 0; e < HD; ++e) dot += qs[wave][e] * __uint_as_float(kr[e]);
-            }
-            s = dot * a.scale;
+        if (nvalid <= 0) continue;  // uniform across the workgroup
+        float qv[Q4];
+        load_row<DType::F32, Q4>(a.Q + (size_t)m * a.n_heads * HD + (size_t)h * HD + qd * Q4, qv);
+        float dot = 0.f;
+#pragma unroll
+        for (int e = 0; e < Q4; ++e) dot += qv[e] * kf[e];
+        dot += __shfl_xor(dot, 16);
+        dot += __shfl_xor(dot, 32);
+        const bool kv_ok = jl < nvalid;
+        const float s = kv_ok ? dot * a.scale : -INFINITY;
+        float mw = s;
+#pragma unroll
+        for (int o = 1; o < 16; o <<= 1) mw = fmaxf(mw, __shfl_xor(mw, o));
+        if (lane == 0) red_m[w] = mw;
+        __syncthreads();
+        const float M = fmaxf(fmaxf(red_m[0], red_m[1]), fmaxf(red_m[2], red_m[3]));
+        const float pj = kv_ok ? expf(s - M) : 0.f;
+        float lw = pj;
+#pragma unroll
+        for (int o = 1; o < 16; o <<= 1) lw += __shfl_xor(lw, o);
+        if (lane == 0) red_l[w] = lw;
+        float o[EPV];
+#pragma unroll
+        for (int q = 0; q < EPV; ++q) o[q] = 0.f;
+        const int nkw = min(16, nvalid - 16 * w);
+#pragma unroll
+        for (int jj = 0; jj < 16; ++jj) {
+            const float pw = __shfl(pj, jj);
+            if (jj < nkw)
+#pragma unroll
+                for (int q = 0; q < EPV; ++q) o[q] += pw * vf[jj][q];
         }
-        const float mx = wave_max(s);
-        const float pj = (lane < nvalid) ? expf(s - mx) : 0.f;
-        const float l = wave_sum(pj);
-        ps[wave][lane] = pj;
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-
-        const size_t slot = ((size_t)m * a.n_heads + h) * a.chunk_stride + ch;
-        constexpr int PER = HD / 64;
-        float o[PER];
 #pragma unroll
-        for (int q = 0; q < PER; ++q) o[q] = 0.f;
-        for (int j = 0; j < nvalid; ++j) {
-            const float pw = ps[wave][j];
+        for (int q = 0; q < EPV; ++q) ow[w][lane * EPV + q] = o[q];
+        __syncthreads();
+        if (w == 0) {
+            const float L = ((red_l[0] + red_l[1]) + red_l[2]) + red_l[3];
+            const size_t slot = ((size_t)m * a.n_heads + h) * a.chunk_stride + ch;
 #pragma unroll
-            for (int q = 0; q < PER; ++q) {
-                const int e = lane + 64 * q;
-                float vv;
-                if (T == DType::BF16) {
-                    const uint32_t wv = Vs[j * (HD / 2) + (e >> 1)];
-                    vv = (e & 1) ? __uint_as_float(wv & 0xffff0000u) : __uint_as_float(wv << 16);
-                } else {
-                    vv = __uint_as_float(Vs[j * HD + e]);
-                }
-                o[q] += pw * vv;
+            for (int q = 0; q < EPV; ++q) {
+                const int e = lane * EPV + q;
+                a.part_o[slot * HD + e] = ((ow[0][e] + ow[1][e]) + ow[2][e]) + ow[3][e];
+            }
+            if (lane == 0) {
+                a.part_ml[slot * 2 + 0] = M;
+                a.part_ml[slot * 2 + 1] = L;
             }
         }
-#pragma unroll
-        for (int q = 0; q < PER; ++q) a.part_o[slot * HD + lane + 64 * q] = o[q];
-        if (lane == 0) {
-            a.part_ml[slot * 2 + 0] = mx;
-            a.part_ml[slot * 2 + 1] = l;
-        }
-        __builtin_amdgcn_wave_barrier();
+        __syncthreads();
     }
 }
 
+// Merge each row's chunk partials in chunk order: one wave per (token, head).
 template <DType T, int HD>
 __global__ void __launch_bounds__(256) attn_combine_kernel(AttnArgs a, int M) {
     const int lane = threadIdx.x & 63;
@@ -512,7 +698,7 @@ __global__ void __launch_bounds__(256) attn_combine_kernel(AttnArgs a, int M) {
     }
 #pragma unroll
     for (int q = 0; q < PER; ++q)
-        St<T>::store(a.O, (size_t)m * a.n_heads * HD + (size_t)h * HD + lane + 64 * q, o[q] / L);
+        St<T>::store(a.O, fm_index<T>(m, h * HD + lane + 64 * q, a.n_heads * HD), o[q] / L);
 }
 
 template <DType T, int HD>
@@ -534,27 +720,8 @@ void launch_attention(DType t, const AttnArgs &a, hipStream_t s) {
 }
 
 // ------------------------------------------------------------------------------------------
-// LoRA u = B_s x, argmax over tile partials
+// argmax over tile partials
 // ------------------------------------------------------------------------------------------
-template <DType T>
-__global__ void __launch_bounds__(256) lora_u_kernel(const void *x, const float *Bm, int d, int r, float *u) {
-    const int m = blockIdx.x, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    for (int c = wave; c < r; c += 4) {
-        float s = 0.f;
-        for (int i = lane; i < d; i += 64) s += Bm[(size_t)c * d + i] * St<T>::load(x, (size_t)m * d + i);
-        s = wave_sum(s);
-        if (lane == 0) u[(size_t)m * r + c] = s;
-    }
-}
-
-void launch_lora_u(DType t, const void *x, const float *Bm, int M, int d, int r, float *u, hipStream_t s) {
-    if (M <= 0) return;
-    if (t == DType::BF16)
-        lora_u_kernel<DType::BF16><<<M, 256, 0, s>>>(x, Bm, d, r, u);
-    else
-        lora_u_kernel<DType::F32><<<M, 256, 0, s>>>(x, Bm, d, r, u);
-}
-
 __global__ void __launch_bounds__(256) argmax_kernel(const float *pv, const int32_t *pi, int ntiles, int32_t *out,
                                                      int out_stride, const int32_t *forced, int32_t *flags) {
     __shared__ float sv[4];
@@ -820,10 +987,12 @@ void launch_update_forward(DType t, const UpdateArgs &u, hipStream_t s) {
     launch_lora_u(t, u.Hh, u.Bm, u.n, u.d, u.rank, u.u, s);
     const size_t es = dtype_size(t);
     for (int r0 = 0; r0 < u.n; r0 += 64) {
+        const int rows = min(64, u.n - r0);
+        launch_gather_fm(t, u.Hh, false, 1, r0, rows, u.d, u.xfm, s);
         GemmArgs g{};
         g.W = u.W;
-        g.X = (const uint8_t *)u.Hh + (size_t)r0 * u.d * es;
-        g.M = min(64, u.n - r0);
+        g.X = u.xfm;
+        g.M = rows;
         g.N = u.V;
         g.K = u.d;
         g.Z = u.Z + (size_t)r0 * u.V;
