@@ -19,7 +19,6 @@ using namespace dvi;
 namespace {
 
 constexpr int kMaxRows = 64;   // tokens per GEMM call (four 16-wide MFMA groups)
-constexpr int kChunk = 64;     // attention key chunk
 
 enum State { S_CREATED = 0, S_READY, S_DRAFTED, S_VERIFIED };
 
@@ -49,6 +48,7 @@ struct dvi_ctx {
     dvi_config cfg;
     DType dt;
     size_t es;
+    int s_cap;  // cache positions per (sequence, kv head): max_seq rounded up to a 64-key chunk
     hipStream_t stream;
     std::vector<LayerW> L;
     void *emb, *head;
@@ -59,7 +59,9 @@ struct dvi_ctx {
     // (ss) and dtype(h * g) for the next folded RMSNorm (hg); hk/hk_ss/hk_hg hold the k_spec
     // drafted rows of every sequence (row b*k_spec + j), which the verify then continues.
     // GEMM inputs (hg, act, attn_o, hk_hg, dfm, pfm, ufm) are in the fragment-major layout.
-    float *h, *ss, *q, *hk, *hk_ss, *vlogits, *dlogits, *part_val, *att_po, *att_pml, *lora_u;
+    float *h, *ss, *q, *hk, *hk_ss, *vlogits, *dlogits, *part_val, *lora_u, *att_po, *att_pml;
+    int32_t *att_cnt;
+    int chunk_stride = 0;
     void *hg, *attn_o, *act, *hk_hg, *hk_hat, *dfm, *pfm, *ufm;
     int32_t *part_idx;
     // small device state; io block is one contiguous region copied back at commit
@@ -77,7 +79,6 @@ struct dvi_ctx {
     // host mirror
     int state = S_CREATED;
     int B = 0, k_spec = 0, ar_mode = 0;
-    int chunk_stride = 0;
     std::vector<int32_t> lens_h;
     int ring_valid_h = 0;
     bool device_error = false;
@@ -120,6 +121,7 @@ static dvi_status fail(dvi_ctx *c, dvi_status s, const char *fmt, ...) {
 static size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
 
 static int qkv_rows(const dvi_config &c) { return (c.n_heads + 2 * c.n_kv_heads) * c.head_dim; }
+static int cache_cap(const dvi_config &c) { return (c.max_seq + 63) / 64 * 64; }
 static int m_max(const dvi_config &c) {
     int m = c.max_batch * c.max_k_spec;
     return m > kMaxRows ? m : kMaxRows;
@@ -132,9 +134,9 @@ static size_t layout(dvi_ctx *x, const dvi_config &c, void *base) {
     const size_t d = c.d_model, F = c.ffn_dim, V = c.vocab, qd = (size_t)c.n_heads * c.head_dim;
     const size_t kvd = (size_t)c.n_kv_heads * c.head_dim;
     const size_t M = m_max(c), R = c.buffer_rows, r = c.lora_rank;
+    const size_t cs = ((size_t)c.max_seq + 63) / 64;
     const size_t Bk = (size_t)c.max_batch * c.max_k_spec;
-    const size_t cs = (c.max_seq + kChunk - 1) / kChunk;
-    const size_t cache = (size_t)c.max_batch * kvd * c.max_seq * es;
+    const size_t cache = (size_t)c.max_batch * kvd * cache_cap(c) * es;
     std::vector<LayerW> Ls(c.n_layers);
     for (int l = 0; l < c.n_layers; ++l) {
         Ls[l].wqkv = b.take<void>((size_t)qkv_rows(c) * d * es);
@@ -169,9 +171,10 @@ static size_t layout(dvi_ctx *x, const dvi_config &c, void *base) {
     float *dlogits = b.take<float>((size_t)c.max_batch * V * 4);
     float *part_val = b.take<float>(M * (V / 16) * 4);
     int32_t *part_idx = b.take<int32_t>(M * (V / 16) * 4);
+    float *lora_u = b.take<float>((M > R ? M : R) * r * 4);
     float *att_po = b.take<float>(M * c.n_heads * cs * c.head_dim * 4);
     float *att_pml = b.take<float>(M * c.n_heads * cs * 2 * 4);
-    float *lora_u = b.take<float>((M > R ? M : R) * r * 4);
+    int32_t *att_cnt = b.take<int32_t>((size_t)c.max_batch * c.n_kv_heads * 4);
     int32_t *lens = b.take<int32_t>(c.max_batch * 4);
     int32_t *pending = b.take<int32_t>(c.max_batch * 4);
     int32_t *drafts = b.take<int32_t>(Bk * 4);
@@ -210,7 +213,8 @@ static size_t layout(dvi_ctx *x, const dvi_config &c, void *base) {
         x->hk = hk; x->hk_ss = hk_ss; x->hk_hg = hk_hg; x->hk_hat = hk_hat;
         x->dfm = dfm; x->pfm = pfm; x->ufm = ufm;
         x->vlogits = vlogits; x->dlogits = dlogits; x->part_val = part_val; x->part_idx = part_idx;
-        x->att_po = att_po; x->att_pml = att_pml; x->lora_u = lora_u;
+        x->lora_u = lora_u;
+        x->att_po = att_po; x->att_pml = att_pml; x->att_cnt = att_cnt; x->chunk_stride = (int)cs;
         x->lens = lens; x->pending = pending; x->drafts = drafts; x->targets = targets; x->forced = forced;
         x->max_new = max_new; x->ids = ids; x->copy_list = copy_list; x->ring_state = ring_state; x->io = io;
         x->prow = prow;
@@ -219,7 +223,6 @@ static size_t layout(dvi_ctx *x, const dvi_config &c, void *base) {
         x->upd_Z = upd_Z; x->upd_stats = upd_stats; x->upd_dA = upd_dA; x->upd_du = upd_du; x->upd_dB = upd_dB;
         x->upd_loss = upd_loss; x->upd_u = lora_u;
         x->mA = mA; x->vA = vA; x->mB = mB; x->vB = vB;
-        x->chunk_stride = (int)cs;
     }
     return align_up(b.off);
 }
@@ -238,6 +241,7 @@ static const char *check_config(const dvi_config *c) {
     if (c->vocab <= 0 || c->vocab % 16) return "vocab must be a positive multiple of 16";
     if (c->max_batch < 1 || c->max_k_spec < 1 || c->max_k_spec > 16) return "max_batch >= 1, 1 <= max_k_spec <= 16";
     if (c->max_batch * c->max_k_spec > kMaxRows) return "max_batch * max_k_spec must be <= 64";
+    if (c->max_batch > dvi::kMaxBatch) return "max_batch must be <= 64";
     if (c->max_seq < 2) return "max_seq < 2";
     if (c->lora_rank < 1 || c->lora_rank > 64) return "lora_rank must be in [1, 64]";
     if (c->buffer_rows < 1) return "buffer_rows < 1";
@@ -290,6 +294,7 @@ extern "C" dvi_status dvi_create(const dvi_config *cfg, const dvi_weights *w, vo
     x->cfg = *cfg;
     x->dt = cfg->dtype == DVI_BF16 ? DType::BF16 : DType::F32;
     x->es = dtype_size(x->dt);
+    x->s_cap = cache_cap(*cfg);
     x->stream = (hipStream_t)stream;
     layout(x, *cfg, ws);
     x->lora_A = w->lora_A;
@@ -369,7 +374,7 @@ extern "C" dvi_status dvi_create(const dvi_config *cfg, const dvi_weights *w, vo
             {x->lens, (size_t)c.max_batch * 4}, {x->pending, (size_t)c.max_batch * 4}, {x->drafts, Bk * 4},
             {x->targets, Bk * 4}, {x->io, (Bk + 2 * (size_t)c.max_batch + 4) * 4}, {x->ring_state, 16},
             {x->ring_fresh, R}, {x->ring_r, R}, {x->mA, (size_t)V * r * 4}, {x->vA, (size_t)V * r * 4},
-            {x->mB, r * d * 4}, {x->vB, r * d * 4}};
+            {x->mB, r * d * 4}, {x->vB, r * d * 4}, {x->att_cnt, (size_t)c.max_batch * c.n_kv_heads * 4}};
         for (const Z &z : zs)
             if (hipMemset(z.p, 0, z.n) != hipSuccess) {
                 *out = x;
@@ -477,26 +482,27 @@ static dvi_status run_layers(dvi_ctx *x, int l0, int l1, int B, int c, int pos_o
         a.n_heads = H;
         a.n_kv = Hkv;
         a.hd = hd;
-        a.s_max = cf.max_seq;
+        a.s_max = x->s_cap;
         a.rope = x->rope;
         gemm(x, EPI_QKV, DVI_PROBE_QKV, Lw.wqkv, hg, M, qkv_rows(cf), d, a);
         AttnArgs at{};
         at.Q = x->q;
         at.Kc = Lw.Kc;
         at.Vc = Lw.Vc;
-        at.lens = x->lens;
+        for (int b = 0; b < B; ++b) at.len[b] = x->lens_h[b];
         at.B = B;
         at.c = c;
         at.pos_off = pos_off;
         at.n_heads = H;
         at.n_kv = Hkv;
         at.hd = hd;
-        at.s_max = cf.max_seq;
-        at.n_chunks = pmax / kChunk + 1;
-        at.chunk_stride = x->chunk_stride;
+        at.s_max = x->s_cap;
         at.scale = 1.0f / sqrtf((float)hd);
+        at.n_chunks = pmax / 64 + 1;
+        at.chunk_stride = x->chunk_stride;
         at.part_o = x->att_po;
         at.part_ml = x->att_pml;
+        at.counters = x->att_cnt;
         at.O = x->attn_o;
         const bool pa = probe_begin(x, DVI_PROBE_ATTENTION);
         launch_attention(x->dt, at, x->stream);
@@ -882,15 +888,25 @@ extern "C" dvi_status dvi_read_kv(dvi_ctx *x, int32_t layer, int32_t seq, int32_
     if (layer < 0 || layer >= cf.n_layers || seq < 0 || seq >= cf.max_batch || pos0 < 0 || npos < 0 ||
         pos0 + npos > cf.max_seq)
         return fail(x, DVI_ERR_ARG, "read_kv range");
-    const size_t row = (size_t)cf.head_dim * x->es;
+    const size_t es = x->es, hd = cf.head_dim, row = hd * es, cap = x->s_cap;
+    std::vector<uint8_t> vt((size_t)cf.n_kv_heads * hd * npos * es);
     for (int h = 0; h < cf.n_kv_heads; ++h) {
-        const size_t off = (((size_t)seq * cf.n_kv_heads + h) * cf.max_seq + pos0) * row;
+        const size_t off = (((size_t)seq * cf.n_kv_heads + h) * cap + pos0) * row;
         HIPCHK(x, hipMemcpyAsync((uint8_t *)k + (size_t)h * npos * row, (uint8_t *)x->L[layer].Kc + off, npos * row,
                                  hipMemcpyDeviceToHost, x->stream));
-        HIPCHK(x, hipMemcpyAsync((uint8_t *)v + (size_t)h * npos * row, (uint8_t *)x->L[layer].Vc + off, npos * row,
-                                 hipMemcpyDeviceToHost, x->stream));
+        // values are stored transposed ([head dim][position]); fetch the [hd, npos] block
+        const size_t voff = (((size_t)seq * cf.n_kv_heads + h) * hd * cap + pos0) * es;
+        if (npos > 0)
+            HIPCHK(x, hipMemcpy2DAsync(vt.data() + (size_t)h * hd * npos * es, npos * es,
+                                       (uint8_t *)x->L[layer].Vc + voff, cap * es, npos * es, hd,
+                                       hipMemcpyDeviceToHost, x->stream));
     }
     HIPCHK(x, hipStreamSynchronize(x->stream));
+    for (int h = 0; h < cf.n_kv_heads; ++h)
+        for (int p = 0; p < npos; ++p)
+            for (size_t d = 0; d < hd; ++d)
+                memcpy((uint8_t *)v + (((size_t)h * npos + p) * hd + d) * es,
+                       vt.data() + (((size_t)h * hd + d) * npos + p) * es, es);
     return DVI_OK;
 }
 

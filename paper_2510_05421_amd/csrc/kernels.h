@@ -55,7 +55,8 @@ struct GemmArgs {
     const float *g_next;
     // EPI_QKV
     float *Q;           // [M][n_heads * hd] fp32
-    void *Kc, *Vc;      // this layer's caches [max_batch][n_kv][s_max][hd]
+    void *Kc, *Vc;      // this layer's caches: keys [max_batch][n_kv][s_max][hd], values
+                        // transposed [max_batch][n_kv][hd][s_max]
     int n_heads, n_kv, hd, s_max;
     const float2 *rope; // [s_max][hd/2] (cos, sin)
     // EPI_SWIGLU
@@ -85,17 +86,21 @@ void launch_head_prep(DType t, const float *h, int ldh, const float *ss, int ld_
 void launch_gather_fm(DType t, const void *src, bool src_fm, int rs, int off, int rows, int K, void *dst,
                       hipStream_t s);
 
+constexpr int kMaxBatch = 64;
+
 struct AttnArgs {
     const float *Q;      // [M][n_heads*hd]
-    const void *Kc, *Vc; // [max_batch][n_kv][s_max][hd]
-    const int32_t *lens;
+    const void *Kc;      // [max_batch][n_kv][s_max][hd]
+    const void *Vc;      // [max_batch][n_kv][hd][s_max] (transposed)
+    int len[kMaxBatch];  // cache length of every sequence (passed by value: no dependent load)
     int B, c, pos_off;
     int n_heads, n_kv, hd, s_max;
-    int n_chunks;        // chunks of the longest context in this call
+    int n_chunks;        // 64-key chunks of the longest context in this call
     int chunk_stride;    // partial slots per (token, head) = ceil(s_max / 64)
     float scale;
     float *part_o;       // [M][n_heads][chunk_stride][hd]
     float *part_ml;      // [M][n_heads][chunk_stride][2]
+    int32_t *counters;   // [max_batch][n_kv]; zero between launches (the merging workgroup resets)
     void *O;             // [M][n_heads*hd] out (dtype, FM)
 };
 void launch_attention(DType t, const AttnArgs &a, hipStream_t s);

@@ -296,13 +296,14 @@ __global__ void __launch_bounds__(64 * WMAX) gemm_kernel(GemmArgs a) {
                         float *q = a.Q + (size_t)m * a.n_heads * a.hd + hg * a.hd;
                         q[j] = x0;
                         q[j + half] = x1;
-                    } else {
-                        const bool isk = hg < a.n_heads + a.n_kv;
-                        const int kvh = isk ? hg - a.n_heads : hg - a.n_heads - a.n_kv;
-                        void *cache = isk ? a.Kc : a.Vc;
-                        const size_t base = (((size_t)b * a.n_kv + kvh) * a.s_max + pos) * a.hd;
-                        St<T>::store(cache, base + j, x0);
-                        St<T>::store(cache, base + j + half, x1);
+                    } else if (hg < a.n_heads + a.n_kv) {  // key cache [b][kv][pos][hd]
+                        const size_t base = (((size_t)b * a.n_kv + (hg - a.n_heads)) * a.s_max + pos) * a.hd;
+                        St<T>::store(a.Kc, base + j, x0);
+                        St<T>::store(a.Kc, base + j + half, x1);
+                    } else {  // value cache, transposed: [b][kv][hd][pos]
+                        const size_t base = ((size_t)b * a.n_kv + (hg - a.n_heads - a.n_kv)) * a.hd;
+                        St<T>::store(a.Vc, (base + j) * a.s_max + pos, x0);
+                        St<T>::store(a.Vc, (base + j + half) * a.s_max + pos, x1);
                     }
                 }
             }
@@ -537,185 +538,300 @@ void launch_lora_u(DType t, const void *x, const float *Bm, int M, int d, int r,
 }
 
 // ------------------------------------------------------------------------------------------
-// Block-causal attention against the KV cache, split over fixed 64-position key chunks.
+// Block-causal attention against the KV cache, on MFMA.
 //
-// Workgroup (chunk ch, kv head, sequence b) serves every query row of the block that reads
-// this kv head (c tokens x n_heads/n_kv grouped heads); the row at position p sees keys
-// 0..p.  Wave w owns keys 16w..16w+15 of the chunk: for the scores, lane l holds key
-// 16w + l%16 and head-dim quarter l/16 of it in registers (a quarter-dot per lane, summed
-// over the four quarters by a butterfly); for P.V, lane l holds head dims [l*HD/64, ..) of
-// the wave's 16 values.  Chunk statistics are combined over the four waves in wave order.
-// Keys and values are read once per workgroup straight into registers and reused by every
-// row.  Each chunk's (max, sum, unnormalised output) goes to a partial slot, and
-// attn_combine merges every row's chunks in chunk order.  Chunk boundaries sit at absolute
-// positions, so a row's result does not depend on the other rows in its block.
+// Keys are cut into 64-position chunks at absolute positions; wave w of workgroup x owns chunk
+// 4x + w of one (kv head, sequence).  The query rows that read this kv head (c tokens x
+// n_heads/n_kv grouped heads) are taken 16 at a time as the MFMA row dimension:
+//   S = Q K^T      A = query fragments, B = key fragments read straight from the key cache;
+//   softmax        per row over the chunk's 64 keys: max, p = exp(s - max), sum (fixed tree);
+//   O = P V        P goes through a per-wave LDS tile into A-operand layout; B = value
+//                  fragments read straight from the transposed value cache (positions
+//                  contiguous per head dim).
+// Row at position p sees keys 0..p (block-causal); keys past a row's position, or past the
+// cached length, are masked before the max and multiply as zeros.  Each chunk's (max, sum,
+// unnormalised output) is published with agent-scope relaxed atomic stores; a per-(sequence,
+// kv head) counter then tells the workgroup that finishes last, and that one merges every row's
+// chunks in chunk order, reading them back with agent-scope loads (no cache writeback, no
+// waiting).  Rows are independent MFMA rows and the chunk arithmetic depends only on positions,
+// so a row's result is the same whichever other rows share its block.
 // ------------------------------------------------------------------------------------------
-// Load n contiguous elements (n * sizeof(E) a multiple of 16 bytes, 16-byte aligned) as floats.
-template <DType T, int N>
-__device__ __forceinline__ void load_row(const void *p, float *out) {
-    const uint4 *q = (const uint4 *)p;
+__device__ __forceinline__ void st_agent(float *p, float v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_agent(const float *p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Pack EPL floats into one 16-byte MFMA fragment of dtype T.
+template <DType T>
+__device__ __forceinline__ uint4 pack_frag(const float *v) {
+    if (T == DType::BF16) {
+        uint32_t w[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) w[k] = (uint32_t)f2bf(v[2 * k]) | ((uint32_t)f2bf(v[2 * k + 1]) << 16);
+        return uint4{w[0], w[1], w[2], w[3]};
+    }
+    return uint4{__float_as_uint(v[0]), __float_as_uint(v[1]), __float_as_uint(v[2]), __float_as_uint(v[3])};
+}
+
+// Zero the elements of a 16-byte value fragment whose key index (first + e) is >= limit.
+template <DType T>
+__device__ __forceinline__ uint4 mask_keys(uint4 v, int first, int limit) {
+    uint32_t w[4] = {v.x, v.y, v.z, v.w};
     if (T == DType::BF16) {
 #pragma unroll
-        for (int i = 0; i < N / 8; ++i) {
-            const uint4 v = q[i];
-            const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                out[8 * i + 2 * k] = __uint_as_float(w[k] << 16);
-                out[8 * i + 2 * k + 1] = __uint_as_float(w[k] & 0xffff0000u);
-            }
+        for (int k = 0; k < 4; ++k) {
+            if (first + 2 * k >= limit) w[k] &= 0xffff0000u;
+            if (first + 2 * k + 1 >= limit) w[k] &= 0x0000ffffu;
         }
     } else {
 #pragma unroll
-        for (int i = 0; i < N / 4; ++i) {
-            const uint4 v = q[i];
-            out[4 * i] = __uint_as_float(v.x);
-            out[4 * i + 1] = __uint_as_float(v.y);
-            out[4 * i + 2] = __uint_as_float(v.z);
-            out[4 * i + 3] = __uint_as_float(v.w);
-        }
+        for (int k = 0; k < 4; ++k)
+            if (first + k >= limit) w[k] = 0u;
     }
+    return uint4{w[0], w[1], w[2], w[3]};
 }
 
-template <DType T, int HD>
-__global__ void __launch_bounds__(256) attn_partial_kernel(AttnArgs a) {
+constexpr long kAttnPackWaves = 2048;
+
+template <DType T, int HD, int WPB>
+__global__ void __launch_bounds__(64 * WPB) attn_kernel(AttnArgs a) {
     typedef typename St<T>::type E;
-    constexpr int Q4 = HD / 4;
-    constexpr int EPV = HD / 64;
-    __shared__ float red_m[4], red_l[4];
-    __shared__ float ow[4][HD];
+    constexpr int KC = (T == DType::BF16) ? 32 : 16;   // reduction depth of one fragment step
+    constexpr int EPL = KC / 4;                          // elements per lane per step
+    constexpr int DS = HD / KC;                          // head-dim steps of S = Q K^T
+    constexpr int KS = CK / KC;                          // key steps of O = P V
+    constexpr int DT = HD / 16;                          // 16-wide head-dim tiles of O
+    constexpr int PST = CK + 16 / (int)sizeof(E);        // padded LDS row of P (elements)
+    __shared__ __align__(16) E Ps[WPB][16][PST];
+    __shared__ int is_last;
 
-    const int ch = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
+    const int kvh = blockIdx.y, b = blockIdx.z;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const int len0 = a.lens[b] + a.pos_off;
+    const int l16 = lane & 15, lg = lane >> 4;
+    const int len0 = a.len[b] + a.pos_off;
     const int pmax = len0 + a.c - 1;
+    const int nch = pmax / CK + 1;
+    if (WPB * (int)blockIdx.x >= nch) return;  // uniform across the workgroup
+    const int ch = WPB * blockIdx.x + w;
+    const bool active = ch < nch;             // uniform across the wave
     const int kbase = ch * CK;
-    if (kbase > pmax) return;
-    const int nk = min(CK, pmax + 1 - kbase);
-    const int jl = 16 * w + (lane & 15);
-    const int qd = lane >> 4;
-    const size_t cache0 = ((size_t)b * a.n_kv + kvh) * a.s_max + kbase;
-
-    float kf[Q4];
-    if (jl < nk) {
-        load_row<T, Q4>((const E *)a.Kc + (cache0 + jl) * HD + qd * Q4, kf);
-    } else {
-#pragma unroll
-        for (int e = 0; e < Q4; ++e) kf[e] = 0.f;
-    }
-    float vf[16][EPV];
-#pragma unroll
-    for (int jj = 0; jj < 16; ++jj) {
-        const int key = 16 * w + jj;
-        const E *vr = (const E *)a.Vc + (cache0 + key) * HD + lane * EPV;
-#pragma unroll
-        for (int q = 0; q < EPV; ++q) vf[jj][q] = key < nk ? St<T>::load(vr, q) : 0.f;
-    }
-
+    const int nk = active ? min(CK, pmax + 1 - kbase) : 0;
     const int G = a.n_heads / a.n_kv;
     const int R = a.c * G;
-    for (int row = 0; row < R; ++row) {
-        const int i = row / G, gi = row - i * G;
-        const int h = kvh * G + gi;
-        const int m = b * a.c + i;
-        const int p = len0 + i;
-        const int nvalid = min(nk, p + 1 - kbase);
-        if (nvalid <= 0) continue;  // uniform across the workgroup
-        float qv[Q4];
-        load_row<DType::F32, Q4>(a.Q + (size_t)m * a.n_heads * HD + (size_t)h * HD + qd * Q4, qv);
-        float dot = 0.f;
-#pragma unroll
-        for (int e = 0; e < Q4; ++e) dot += qv[e] * kf[e];
-        dot += __shfl_xor(dot, 16);
-        dot += __shfl_xor(dot, 32);
-        const bool kv_ok = jl < nvalid;
-        const float s = kv_ok ? dot * a.scale : -INFINITY;
-        float mw = s;
-#pragma unroll
-        for (int o = 1; o < 16; o <<= 1) mw = fmaxf(mw, __shfl_xor(mw, o));
-        if (lane == 0) red_m[w] = mw;
-        __syncthreads();
-        const float M = fmaxf(fmaxf(red_m[0], red_m[1]), fmaxf(red_m[2], red_m[3]));
-        const float pj = kv_ok ? expf(s - M) : 0.f;
-        float lw = pj;
-#pragma unroll
-        for (int o = 1; o < 16; o <<= 1) lw += __shfl_xor(lw, o);
-        if (lane == 0) red_l[w] = lw;
-        float o[EPV];
-#pragma unroll
-        for (int q = 0; q < EPV; ++q) o[q] = 0.f;
-        const int nkw = min(16, nvalid - 16 * w);
-#pragma unroll
-        for (int jj = 0; jj < 16; ++jj) {
-            const float pw = __shfl(pj, jj);
-            if (jj < nkw)
-#pragma unroll
-                for (int q = 0; q < EPV; ++q) o[q] += pw * vf[jj][q];
-        }
-#pragma unroll
-        for (int q = 0; q < EPV; ++q) ow[w][lane * EPV + q] = o[q];
-        __syncthreads();
-        if (w == 0) {
-            const float L = ((red_l[0] + red_l[1]) + red_l[2]) + red_l[3];
-            const size_t slot = ((size_t)m * a.n_heads + h) * a.chunk_stride + ch;
-#pragma unroll
-            for (int q = 0; q < EPV; ++q) {
-                const int e = lane * EPV + q;
-                a.part_o[slot * HD + e] = ((ow[0][e] + ow[1][e]) + ow[2][e]) + ow[3][e];
-            }
-            if (lane == 0) {
-                a.part_ml[slot * 2 + 0] = M;
-                a.part_ml[slot * 2 + 1] = L;
-            }
-        }
-        __syncthreads();
-    }
-}
+    const size_t kc0 = ((size_t)b * a.n_kv + kvh) * a.s_max + kbase;          // key rows
+    const size_t vt0 = ((size_t)b * a.n_kv + kvh) * HD * a.s_max + kbase;      // value columns
+    const uint4 zero = {0u, 0u, 0u, 0u};
 
-// Merge each row's chunk partials in chunk order: one wave per (token, head).
-template <DType T, int HD>
-__global__ void __launch_bounds__(256) attn_combine_kernel(AttnArgs a, int M) {
-    const int lane = threadIdx.x & 63;
-    const int item = blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (item >= M * a.n_heads) return;
-    const int m = item / a.n_heads, h = item - m * a.n_heads;
-    const int b = m / a.c, i = m - b * a.c;
-    const int p = a.lens[b] + a.pos_off + i;
-    const int nch = p / CK + 1;
-    const size_t slot0 = ((size_t)m * a.n_heads + h) * a.chunk_stride;
-    float M_ = -INFINITY;
-    for (int ch = 0; ch < nch; ++ch) M_ = fmaxf(M_, a.part_ml[(slot0 + ch) * 2]);
-    float L = 0.f;
+    if (active) {
+        // Every position of a 64-key chunk lies inside the cache row (the row length is a multiple
+        // of 64), so the fragment loads are unconditional; keys at or past nk (not yet written,
+        // or past the block) are zeroed afterwards.
+        // key fragments: tile t holds keys 16t + l16; head dims step*KC + EPL*lg .. +EPL
+        uint4 kf[4][DS];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            const int key = 16 * t + l16;
+            const uint4 *src = (const uint4 *)((const E *)a.Kc + (kc0 + key) * HD + EPL * lg);
+#pragma unroll
+            for (int st = 0; st < DS; ++st) {
+                const uint4 v = src[st * (KC * sizeof(E) / 16)];
+                kf[t][st] = key < nk ? v : zero;
+            }
+        }
+        // value fragments: tile dt holds head dim 16 dt + l16; keys step*KC + EPL*lg .. +EPL
+        uint4 vf[DT][KS];
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+            const E *src = (const E *)a.Vc + vt0 + (size_t)(16 * dt + l16) * a.s_max + EPL * lg;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks)
+                vf[dt][ks] = mask_keys<T>(*(const uint4 *)(src + ks * KC), ks * KC + EPL * lg, nk);
+        }
+        for (int r0 = 0; r0 < R; r0 += 16) {
+            // query fragments: row r0 + l16, head dims step*KC + EPL*lg .. +EPL
+            const int rq = r0 + l16;
+            uint4 qf[DS];
+            {
+                const bool ok = rq < R;
+                const int rr = ok ? rq : R - 1;  // rows past R read row R-1 and are zeroed
+                const int i = rr / G, gi = rr - i * G;
+                const float4 *qrow =
+                    (const float4 *)(a.Q + ((size_t)(b * a.c + i) * a.n_heads + kvh * G + gi) * HD + EPL * lg);
+#pragma unroll
+                for (int st = 0; st < DS; ++st) {
+                    float v[EPL];
+#pragma unroll
+                    for (int e4 = 0; e4 < EPL / 4; ++e4) {
+                        const float4 q4 = qrow[(st * KC) / 4 + e4];
+                        v[4 * e4 + 0] = ok ? q4.x : 0.f;
+                        v[4 * e4 + 1] = ok ? q4.y : 0.f;
+                        v[4 * e4 + 2] = ok ? q4.z : 0.f;
+                        v[4 * e4 + 3] = ok ? q4.w : 0.f;
+                    }
+                    qf[st] = pack_frag<T>(v);
+                }
+            }
+            // S: lane holds rows r0 + 4 lg + j, key 16 t + l16
+            f32x4 S[4];
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                S[t] = (f32x4){0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int st = 0; st < DS; ++st) S[t] = St<T>::mma(qf[st], kf[t][st], S[t]);
+            }
+            float rmax[4], rsum[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int r = r0 + 4 * lg + j;
+                const int i = r / G;
+                const int nvalid = r < R ? min(nk, len0 + i + 1 - kbase) : 0;
+                float mx = -INFINITY;
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    const float sv = (16 * t + l16 < nvalid) ? S[t][j] * a.scale : -INFINITY;
+                    S[t][j] = sv;
+                    mx = fmaxf(mx, sv);
+                }
+#pragma unroll
+                for (int o = 1; o < 16; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+                float ps = 0.f;
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    const float pv = (mx == -INFINITY) ? 0.f : expf(S[t][j] - mx);
+                    S[t][j] = pv;
+                    ps += pv;
+                }
+#pragma unroll
+                for (int o = 1; o < 16; o <<= 1) ps += __shfl_xor(ps, o);
+                rmax[j] = mx;
+                rsum[j] = ps;
+            }
+            // P -> LDS (row-major, dtype), then read back as A fragments
+#pragma unroll
+            for (int t = 0; t < 4; ++t)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) St<T>::store(&Ps[w][4 * lg + j][0], 16 * t + l16, S[t][j]);
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            uint4 pf[KS];
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) pf[ks] = *(const uint4 *)&Ps[w][l16][ks * KC + EPL * lg];
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            // O: lane holds rows r0 + 4 lg + j, head dim 16 dt + l16
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) {
+                f32x4 O = (f32x4){0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks) O = St<T>::mma(pf[ks], vf[dt][ks], O);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int r = r0 + 4 * lg + j;
+                    if (r < R && rmax[j] != -INFINITY) {
+                        const int i = r / G, gi = r - i * G;
+                        const size_t slot = ((size_t)(b * a.c + i) * a.n_heads + kvh * G + gi) * a.chunk_stride + ch;
+                        st_agent(a.part_o + slot * HD + 16 * dt + l16, O[j]);
+                        if (dt == 0 && l16 == 0) {
+                            st_agent(a.part_ml + slot * 2 + 0, rmax[j]);
+                            st_agent(a.part_ml + slot * 2 + 1, rsum[j]);
+                        }
+                    }
+                }
+            }
+        }
+    }
+
+    // The workgroup that finishes last for (b, kv head) merges every row's chunks.
+    __builtin_amdgcn_s_waitcnt(0);  // this workgroup's partial stores have completed
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const int nwg = (nch + WPB - 1) / WPB;
+        const int old = __hip_atomic_fetch_add(a.counters + b * a.n_kv + kvh, 1, __ATOMIC_RELAXED,
+                                               __HIP_MEMORY_SCOPE_AGENT);
+        is_last = (old == nwg - 1);
+        if (is_last)
+            __hip_atomic_store(a.counters + b * a.n_kv + kvh, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __syncthreads();
+    if (!is_last) return;
+    // Merge, one wave per row.  Chunks are taken 64 at a time, lane = chunk: the group's
+    // maximum and the rescaled sums come from wave reductions with a fixed tree, and the partial
+    // outputs are folded in chunk order.  All loads are unconditional (addresses clamped to the
+    // row's last chunk, weights of clamped lanes zero) and issued before the arithmetic that
+    // needs them, so a row with up to 64 chunks costs one round trip.
     constexpr int PER = HD / 64;
-    float o[PER];
+    for (int row = w; row < R; row += WPB) {
+        const int i = row / G, gi = row - i * G;
+        const int m = b * a.c + i, h = kvh * G + gi;
+        const int ncr = (len0 + i) / CK + 1;
+        const size_t slot0 = ((size_t)m * a.n_heads + h) * a.chunk_stride;
+        float Mr = -INFINITY, L = 0.f, o[PER];
 #pragma unroll
-    for (int q = 0; q < PER; ++q) o[q] = 0.f;
-    for (int ch = 0; ch < nch; ++ch) {
-        const float sc = expf(a.part_ml[(slot0 + ch) * 2] - M_);
-        L += a.part_ml[(slot0 + ch) * 2 + 1] * sc;
+        for (int q = 0; q < PER; ++q) o[q] = 0.f;
+        for (int c0 = 0; c0 < ncr; c0 += 64) {
+            const int cn = min(64, ncr - c0);
+            const size_t sl = slot0 + c0 + min(lane, cn - 1);
+            const float my_m = ld_agent(a.part_ml + sl * 2), my_l = ld_agent(a.part_ml + sl * 2 + 1);
+            float ov[8][PER];
 #pragma unroll
-        for (int q = 0; q < PER; ++q) o[q] += a.part_o[(slot0 + ch) * HD + lane + 64 * q] * sc;
+            for (int u = 0; u < 8; ++u)
+#pragma unroll
+                for (int q = 0; q < PER; ++q)
+                    ov[u][q] = ld_agent(a.part_o + (slot0 + c0 + min(u, cn - 1)) * HD + lane + 64 * q);
+            const float gm = wave_max(lane < cn ? my_m : -INFINITY);
+            const float Mn = fmaxf(Mr, gm);
+            const float rs = expf(Mr - Mn);  // 0 on the first group
+            const float scl = lane < cn ? expf(my_m - Mn) : 0.f;
+            L = L * rs + wave_sum(my_l * scl);
+#pragma unroll
+            for (int q = 0; q < PER; ++q) o[q] *= rs;
+            Mr = Mn;
+            for (int cb = 0; cb < cn; cb += 8) {
+                if (cb > 0) {
+#pragma unroll
+                    for (int u = 0; u < 8; ++u)
+#pragma unroll
+                        for (int q = 0; q < PER; ++q)
+                            ov[u][q] = ld_agent(a.part_o + (slot0 + c0 + min(cb + u, cn - 1)) * HD + lane + 64 * q);
+                }
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    const float sc = __shfl(scl, cb + u);  // zero for chunks past cn
+#pragma unroll
+                    for (int q = 0; q < PER; ++q) o[q] += ov[u][q] * sc;
+                }
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < PER; ++q)
+            St<T>::store(a.O, fm_index<T>(m, h * HD + lane + 64 * q, a.n_heads * HD), o[q] / L);
     }
-#pragma unroll
-    for (int q = 0; q < PER; ++q)
-        St<T>::store(a.O, fm_index<T>(m, h * HD + lane + 64 * q, a.n_heads * HD), o[q] / L);
 }
 
 template <DType T, int HD>
-static void attn_launch(const AttnArgs &a, hipStream_t s) {
-    dim3 grid(a.n_chunks, a.n_kv, a.B);
-    attn_partial_kernel<T, HD><<<grid, 256, 0, s>>>(a);
-    const int M = a.B * a.c;
-    attn_combine_kernel<T, HD><<<(M * a.n_heads + 3) / 4, 256, 0, s>>>(a, M);
+static void launch_attention_t(const AttnArgs &a, hipStream_t s) {
+    // One wave per 64-key chunk, four chunks per workgroup: the workgroup that finishes last
+    // merges with four waves.  A single query row per kv head over a small grid takes one wave
+    // per workgroup instead, which spreads the chunks over more compute units.
+    const long waves = (long)a.n_chunks * a.n_kv * a.B;
+    if (a.c * (a.n_heads / a.n_kv) == 1 && waves < kAttnPackWaves) {
+        attn_kernel<T, HD, 1><<<dim3(a.n_chunks, a.n_kv, a.B), 64, 0, s>>>(a);
+    } else {
+        attn_kernel<T, HD, 4><<<dim3((a.n_chunks + 3) / 4, a.n_kv, a.B), 256, 0, s>>>(a);
+    }
 }
 
 void launch_attention(DType t, const AttnArgs &a, hipStream_t s) {
     if (t == DType::BF16) {
-        if (a.hd == 128) attn_launch<DType::BF16, 128>(a, s);
-        else attn_launch<DType::BF16, 64>(a, s);
+        if (a.hd == 128) launch_attention_t<DType::BF16, 128>(a, s);
+        else launch_attention_t<DType::BF16, 64>(a, s);
     } else {
-        if (a.hd == 128) attn_launch<DType::F32, 128>(a, s);
-        else attn_launch<DType::F32, 64>(a, s);
+        if (a.hd == 128) launch_attention_t<DType::F32, 128>(a, s);
+        else launch_attention_t<DType::F32, 64>(a, s);
     }
 }
 
