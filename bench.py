@@ -30,7 +30,8 @@ PAPER_CONTEXT = ("paper: 2.16x average wall-time speedup over greedy AR decoding
                  "(Vicuna-7B, Spec-Bench, split k=2, k_spec=4); no absolute tokens/s published")
 KERNEL_NAMES = {"gate_up": "gemm_kernel<bf16,MG=1,EPI_SWIGLU> (gate/up projection, SwiGLU epilogue)",
                 "qkv": "gemm_kernel<bf16,MG=1,EPI_QKV>", "down": "gemm_kernel<bf16,MG=1,EPI_RESID> (MLP down)",
-                "head": "gemm_kernel<bf16,MG=1,EPI_LOGITS>", "attention": "attn_partial+attn_combine"}
+                "head": "gemm_kernel<bf16,MG=1,EPI_LOGITS>",
+                "attention": "attn_kernel<bf16,128> (split-KV MFMA attention with in-kernel merge)"}
 
 
 def log(msg):
@@ -63,18 +64,31 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-ar", action="store_true")
+    ap.add_argument("--copy-calib-mib", type=int, default=0,
+                    help="first run 3 plain device-to-device copies of this many MiB (a reference for "
+                         "the hardware byte counters under a profiler)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU only: this build runs the decode step on a single MI355X "
-              "(no multi-GPU path); run with --gpus 1", file=sys.stderr)
+        print("bench.py measures one GPU only: the decode step runs on a single MI355X "
+              "(there is no multi-GPU path); run with --gpus 1", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
     import torch
     import synth
     from paper_2510_05421_amd.engine import Engine, EngineConfig
+
+    if args.copy_calib_mib > 0:
+        n = args.copy_calib_mib << 20
+        src = torch.empty(n, dtype=torch.uint8, device="cuda:0").fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log("copy calibration: 3 device copies of %d bytes" % n)
+        del src, dst
 
     wl = synth.WORKLOADS[args.workload]
     shape = wl.model

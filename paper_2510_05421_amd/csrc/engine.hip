@@ -410,16 +410,21 @@ extern "C" const char *dvi_last_error(const dvi_ctx *x) { return x ? x->err : "n
 // ------------------------------------------------------------------------------------------
 constexpr size_t kProbeMax = 8192;
 
-static bool probe_begin(dvi_ctx *x, int cls) {
-    if (x->probe != cls || x->pused + 2 > x->pev.size()) return false;
-    return hipEventRecord(x->pev[x->pused], x->stream) == hipSuccess;
-}
-static void probe_end(dvi_ctx *x, double bytes) {
-    if (hipEventRecord(x->pev[x->pused + 1], x->stream) == hipSuccess) {
-        x->pused += 2;
-        x->plaunch += 1;
-        x->pbytes += bytes;
+// The probed kernel class is launched with a start/stop event pair that the launch itself
+// stamps at the kernel's start and end.
+static LaunchEvents probe_begin(dvi_ctx *x, int cls) {
+    LaunchEvents ev;
+    if (x->probe == cls && x->pused + 2 <= x->pev.size()) {
+        ev.start = x->pev[x->pused];
+        ev.stop = x->pev[x->pused + 1];
     }
+    return ev;
+}
+static void probe_end(dvi_ctx *x, const LaunchEvents &ev, double bytes) {
+    if (!ev.start) return;
+    x->pused += 2;
+    x->plaunch += 1;
+    x->pbytes += bytes;
 }
 
 // Algorithmic bytes of one GEMM launch: the weight matrix once, activations in, results out.
@@ -442,9 +447,9 @@ static void gemm(dvi_ctx *x, Epi e, int cls, const void *W, const void *X, int M
     a.M = M;
     a.N = N;
     a.K = K;
-    const bool pr = probe_begin(x, cls);
-    launch_gemm(x->dt, e, a, x->stream);
-    if (pr) probe_end(x, gemm_bytes(x, e, M, N, K));
+    const LaunchEvents ev = probe_begin(x, cls);
+    launch_gemm(x->dt, e, a, x->stream, ev);
+    probe_end(x, ev, gemm_bytes(x, e, M, N, K));
 }
 
 // Layers [l0, l1) on M = B*c rows; row r = b*c+i sits at position lens[b] + pos_off + i.  The
@@ -504,13 +509,13 @@ static dvi_status run_layers(dvi_ctx *x, int l0, int l1, int B, int c, int pos_o
         at.part_ml = x->att_pml;
         at.counters = x->att_cnt;
         at.O = x->attn_o;
-        const bool pa = probe_begin(x, DVI_PROBE_ATTENTION);
-        launch_attention(x->dt, at, x->stream);
-        if (pa) {
+        const LaunchEvents ev = probe_begin(x, DVI_PROBE_ATTENTION);
+        launch_attention(x->dt, at, x->stream, ev);
+        if (ev.start) {
             // keys and values of positions 0..p read once per (sequence, kv head); q in, o out
             double kv = 0.0;
             for (int b = 0; b < B; ++b) kv += (double)(x->lens_h[b] + pos_off + c) * Hkv * hd * 2.0 * x->es;
-            probe_end(x, kv + (double)M * H * hd * (4.0 + x->es));
+            probe_end(x, ev, kv + (double)M * H * hd * (4.0 + x->es));
         }
         GemmArgs r{};
         r.H = h;

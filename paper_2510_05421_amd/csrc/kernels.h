@@ -70,7 +70,14 @@ struct GemmArgs {
     float *part_val;    // [M][N/16]
     int32_t *part_idx;  // [M][N/16]
 };
-void launch_gemm(DType t, Epi e, const GemmArgs &a, hipStream_t s);
+// Optional start/stop events for one launch: when set, the kernel is launched with
+// hipExtLaunchKernelGGL, which stamps the events at the kernel's own start and end (the same
+// interval a kernel-trace profiler reports), instead of with separate event markers.
+struct LaunchEvents {
+    hipEvent_t start = nullptr, stop = nullptr;
+};
+
+void launch_gemm(DType t, Epi e, const GemmArgs &a, hipStream_t s, const LaunchEvents &ev = {});
 
 // Row m = b*c + i: h = E[tok[b*tok_stride + i]] (fp32, row stride ldh), its per-16-column
 // sums of squares (ss, stride ld_ss) and dtype(h * g) (hg, FM, row m).
@@ -103,7 +110,7 @@ struct AttnArgs {
     int32_t *counters;   // [max_batch][n_kv]; zero between launches (the merging workgroup resets)
     void *O;             // [M][n_heads*hd] out (dtype, FM)
 };
-void launch_attention(DType t, const AttnArgs &a, hipStream_t s);
+void launch_attention(DType t, const AttnArgs &a, hipStream_t s, const LaunchEvents &ev = {});
 
 // u[m][c] = sum_i B[c][i] * x[m][i]   (x dtype, B fp32 [r][d])
 void launch_lora_u(DType t, const void *x, const float *Bm, int M, int d, int r, float *u, hipStream_t s);

@@ -8,6 +8,8 @@
 // identical to plain greedy decoding on the same engine.
 #include "kernels.h"
 
+#include <hip/hip_ext.h>
+
 #include <math.h>
 
 namespace dvi {
@@ -382,47 +384,57 @@ static GemmShape gemm_shape(int N, int K, int KC, int M) {
     return {rt, w};
 }
 
+template <typename Arg>
+static void launch_timed(void (*kernel)(Arg), dim3 grid, dim3 block, hipStream_t s, const LaunchEvents &ev,
+                         const Arg &a) {
+    if (ev.start)
+        hipExtLaunchKernelGGL(kernel, grid, block, 0, s, ev.start, ev.stop, 0, a);
+    else
+        kernel<<<grid, block, 0, s>>>(a);
+}
+
 template <DType T, int EPI, int RT, int WMAX>
-static void gemm_dispatch_mg(const GemmArgs &a, dim3 grid, dim3 block, hipStream_t s) {
+static void gemm_dispatch_mg(const GemmArgs &a, dim3 grid, dim3 block, hipStream_t s, const LaunchEvents &ev) {
     const int mg = (a.M + 15) / 16;
     switch (mg) {
-        case 1: gemm_kernel<T, 1, EPI, RT, WMAX><<<grid, block, 0, s>>>(a); break;
-        case 2: gemm_kernel<T, 2, EPI, RT, WMAX><<<grid, block, 0, s>>>(a); break;
-        case 3: gemm_kernel<T, 3, EPI, RT, WMAX><<<grid, block, 0, s>>>(a); break;
-        default: gemm_kernel<T, 4, EPI, RT, WMAX><<<grid, block, 0, s>>>(a); break;
+        case 1: launch_timed(gemm_kernel<T, 1, EPI, RT, WMAX>, grid, block, s, ev, a); break;
+        case 2: launch_timed(gemm_kernel<T, 2, EPI, RT, WMAX>, grid, block, s, ev, a); break;
+        case 3: launch_timed(gemm_kernel<T, 3, EPI, RT, WMAX>, grid, block, s, ev, a); break;
+        default: launch_timed(gemm_kernel<T, 4, EPI, RT, WMAX>, grid, block, s, ev, a); break;
     }
 }
 
 template <DType T, int RT, int WMAX>
-static void gemm_dispatch_epi(Epi e, const GemmArgs &a, dim3 grid, dim3 block, hipStream_t s) {
+static void gemm_dispatch_epi(Epi e, const GemmArgs &a, dim3 grid, dim3 block, hipStream_t s,
+                              const LaunchEvents &ev) {
     switch (e) {
-        case EPI_RESID: gemm_dispatch_mg<T, EPI_RESID, RT, WMAX>(a, grid, block, s); break;
-        case EPI_QKV: gemm_dispatch_mg<T, EPI_QKV, RT, WMAX>(a, grid, block, s); break;
-        case EPI_SWIGLU: gemm_dispatch_mg<T, EPI_SWIGLU, RT, WMAX>(a, grid, block, s); break;
-        default: gemm_dispatch_mg<T, EPI_LOGITS, RT, WMAX>(a, grid, block, s); break;
+        case EPI_RESID: gemm_dispatch_mg<T, EPI_RESID, RT, WMAX>(a, grid, block, s, ev); break;
+        case EPI_QKV: gemm_dispatch_mg<T, EPI_QKV, RT, WMAX>(a, grid, block, s, ev); break;
+        case EPI_SWIGLU: gemm_dispatch_mg<T, EPI_SWIGLU, RT, WMAX>(a, grid, block, s, ev); break;
+        default: gemm_dispatch_mg<T, EPI_LOGITS, RT, WMAX>(a, grid, block, s, ev); break;
     }
 }
 
 template <DType T>
-static void gemm_dispatch(Epi e, const GemmArgs &a, GemmShape sh, hipStream_t s) {
+static void gemm_dispatch(Epi e, const GemmArgs &a, GemmShape sh, hipStream_t s, const LaunchEvents &ev) {
     dim3 grid(a.N / 16 / sh.rt), block(64 * sh.waves);
     if (sh.waves > 8) {
-        gemm_dispatch_epi<T, 1, 16>(e, a, grid, block, s);
+        gemm_dispatch_epi<T, 1, 16>(e, a, grid, block, s, ev);
         return;
     }
     switch (sh.rt) {
-        case 4: gemm_dispatch_epi<T, 4, 8>(e, a, grid, block, s); break;
-        case 2: gemm_dispatch_epi<T, 2, 8>(e, a, grid, block, s); break;
-        default: gemm_dispatch_epi<T, 1, 8>(e, a, grid, block, s); break;
+        case 4: gemm_dispatch_epi<T, 4, 8>(e, a, grid, block, s, ev); break;
+        case 2: gemm_dispatch_epi<T, 2, 8>(e, a, grid, block, s, ev); break;
+        default: gemm_dispatch_epi<T, 1, 8>(e, a, grid, block, s, ev); break;
     }
 }
 
-void launch_gemm(DType t, Epi e, const GemmArgs &a, hipStream_t s) {
+void launch_gemm(DType t, Epi e, const GemmArgs &a, hipStream_t s, const LaunchEvents &ev) {
     const GemmShape sh = gemm_shape(a.N, a.K, pack_kc(t), a.M);
     if (t == DType::BF16)
-        gemm_dispatch<DType::BF16>(e, a, sh, s);
+        gemm_dispatch<DType::BF16>(e, a, sh, s, ev);
     else
-        gemm_dispatch<DType::F32>(e, a, sh, s);
+        gemm_dispatch<DType::F32>(e, a, sh, s, ev);
 }
 
 // ------------------------------------------------------------------------------------------
@@ -813,25 +825,25 @@ __global__ void __launch_bounds__(64 * WPB) attn_kernel(AttnArgs a) {
 }
 
 template <DType T, int HD>
-static void launch_attention_t(const AttnArgs &a, hipStream_t s) {
+static void launch_attention_t(const AttnArgs &a, hipStream_t s, const LaunchEvents &ev) {
     // One wave per 64-key chunk, four chunks per workgroup: the workgroup that finishes last
     // merges with four waves.  A single query row per kv head over a small grid takes one wave
     // per workgroup instead, which spreads the chunks over more compute units.
     const long waves = (long)a.n_chunks * a.n_kv * a.B;
     if (a.c * (a.n_heads / a.n_kv) == 1 && waves < kAttnPackWaves) {
-        attn_kernel<T, HD, 1><<<dim3(a.n_chunks, a.n_kv, a.B), 64, 0, s>>>(a);
+        launch_timed(attn_kernel<T, HD, 1>, dim3(a.n_chunks, a.n_kv, a.B), dim3(64), s, ev, a);
     } else {
-        attn_kernel<T, HD, 4><<<dim3((a.n_chunks + 3) / 4, a.n_kv, a.B), 256, 0, s>>>(a);
+        launch_timed(attn_kernel<T, HD, 4>, dim3((a.n_chunks + 3) / 4, a.n_kv, a.B), dim3(256), s, ev, a);
     }
 }
 
-void launch_attention(DType t, const AttnArgs &a, hipStream_t s) {
+void launch_attention(DType t, const AttnArgs &a, hipStream_t s, const LaunchEvents &ev) {
     if (t == DType::BF16) {
-        if (a.hd == 128) launch_attention_t<DType::BF16, 128>(a, s);
-        else launch_attention_t<DType::BF16, 64>(a, s);
+        if (a.hd == 128) launch_attention_t<DType::BF16, 128>(a, s, ev);
+        else launch_attention_t<DType::BF16, 64>(a, s, ev);
     } else {
-        if (a.hd == 128) launch_attention_t<DType::F32, 128>(a, s);
-        else launch_attention_t<DType::F32, 64>(a, s);
+        if (a.hd == 128) launch_attention_t<DType::F32, 128>(a, s, ev);
+        else launch_attention_t<DType::F32, 64>(a, s, ev);
     }
 }
 
