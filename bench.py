@@ -34,6 +34,34 @@ KERNEL_NAMES = {"gate_up": "gemm_kernel<bf16,MG=1,EPI_SWIGLU> (gate/up projectio
                 "attention": "attn_kernel<bf16,128> (split-KV MFMA attention with in-kernel merge)"}
 
 
+# Measured HBM traffic of a probed kernel: the committed summary of two rocprofv3 --pmc passes
+# (FETCH_SIZE, WRITE_SIZE) over this benchmark, scaled by what the same counters read for a
+# plain device copy.  Used only while the kernel source it was taken on is unchanged.
+TRAFFIC_PROFILES = {"gate_up": "profiles/gemm_gate_up_7b_b1_k4_traffic.md"}
+KERNEL_SOURCE = "paper_2510_05421_amd/csrc/kernels.hip"
+
+
+def measured_traffic(probe, workload, k_spec):
+    """Bytes per launch from the committed counter summary, or None when there is none for
+    this kernel and workload or the kernel source has changed since it was taken."""
+    import hashlib
+    rel = TRAFFIC_PROFILES.get(probe)
+    if rel is None or not os.path.exists(os.path.join(ROOT, rel)):
+        return None
+    fields = {}
+    with open(os.path.join(ROOT, rel)) as f:
+        for line in f:
+            if line.startswith("- `") and "`: " in line:
+                key, val = line[3:].split("`: ", 1)
+                fields[key] = val.strip().strip("`")
+    with open(os.path.join(ROOT, KERNEL_SOURCE), "rb") as f:
+        sha = hashlib.sha256(f.read()).hexdigest()
+    if (fields.get("kernels_hip_sha256") != sha or fields.get("workload") != workload
+            or fields.get("k_spec") != str(k_spec)):
+        return None
+    return int(float(fields["traffic_bytes_per_launch"]))
+
+
 def log(msg):
     print("[bench] " + msg, file=sys.stderr, flush=True)
 
@@ -61,7 +89,7 @@ def main():
     ap.add_argument("--probe", default="gate_up", choices=sorted(KERNEL_NAMES))
     ap.add_argument("--probe-steps", type=int, default=20)
     ap.add_argument("--ar-steps", type=int, default=40)
-    ap.add_argument("--cpu-seconds", type=float, default=20.0)
+    ap.add_argument("--cpu-seconds", type=float, default=30.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-ar", action="store_true")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
@@ -183,7 +211,8 @@ def main():
             per_launch = pr["bytes"] / pr["launches"]
             achieved = per_launch / (avg_ms * 1e-3) / 1e9
             roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                    "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                    "frac": round(achieved / HBM_PEAK_GBS, 4),
+                    "traffic": measured_traffic(args.probe, wl.name, k),
                     "kernel": KERNEL_NAMES[args.probe], "launches": pr["launches"],
                     "avg_us": round(avg_ms * 1e3, 2), "bytes_per_launch": int(per_launch)}
             log("probe %s: %d launches, avg %.1f us, %.0f GB/s" % (args.probe, pr["launches"], avg_ms * 1e3,
