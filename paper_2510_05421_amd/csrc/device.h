@@ -1,0 +1,291 @@
+// Device helpers shared by the gfx950 kernels: storage types and MFMA, the fragment-major
+// activation layout, fixed-order reductions, streaming and agent-scope memory accesses, and the
+// fused GEMM epilogues.
+#pragma once
+
+#include "kernels.h"
+
+#include <math.h>
+
+namespace dvi {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(4))) float f32x4;
+
+__device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
+
+__device__ __forceinline__ uint16_t f2bf(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+template <DType T> struct St;
+template <> struct St<DType::F32> {
+    typedef float type;
+    static __device__ __forceinline__ float load(const void *p, size_t i) { return ((const float *)p)[i]; }
+    static __device__ __forceinline__ void store(void *p, size_t i, float v) { ((float *)p)[i] = v; }
+    // D += A * B over one 1 KiB fragment pair: four 16x16x4 fp32 MFMAs, element e of each
+    // lane's 16 bytes going to MFMA e (A and B use the same k assignment).
+    static __device__ __forceinline__ f32x4 mma(uint4 a, uint4 b, f32x4 c) {
+        c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y), c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z), c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), c, 0, 0, 0);
+        return c;
+    }
+};
+template <> struct St<DType::BF16> {
+    typedef uint16_t type;
+    static __device__ __forceinline__ float load(const void *p, size_t i) { return bf2f(((const uint16_t *)p)[i]); }
+    static __device__ __forceinline__ void store(void *p, size_t i, float v) { ((uint16_t *)p)[i] = f2bf(v); }
+    static __device__ __forceinline__ f32x4 mma(uint4 a, uint4 b, f32x4 c) {
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b),
+                                                       c, 0, 0, 0);
+    }
+};
+
+// Fragment-major activation layout ("FM"): the input X[M][K] of a GEMM is stored as, for each
+// 16-token group g and K chunk c (KC columns), one contiguous 1 KiB block whose 16-byte lane
+// slot l holds X[16g + l%16][c*KC + (l/16)*EPL .. +EPL) -- exactly the MFMA B fragment of
+// lane l.  Element (m, k) of a K-column matrix therefore sits at fm_index(m, k, K).
+template <DType T>
+__device__ __forceinline__ size_t fm_index(int m, int k, int K) {
+    constexpr int KC = (T == DType::BF16) ? 32 : 16, EPL = KC / 4;
+    const int c = k / KC, rr = k - c * KC, G = rr / EPL, e = rr - G * EPL;
+    return ((size_t)((m >> 4) * (K / KC) + c) * 64 + G * 16 + (m & 15)) * EPL + e;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+    return v;
+}
+
+// Block-wide sum of 256 threads in a fixed order: butterfly inside each wave, then waves 0..3.
+__device__ __forceinline__ float block_sum256(float v, float *lds4) {
+    v = wave_sum(v);
+    const int w = threadIdx.x >> 6;
+    __syncthreads();
+    if ((threadIdx.x & 63) == 0) lds4[w] = v;
+    __syncthreads();
+    return ((lds4[0] + lds4[1]) + lds4[2]) + lds4[3];
+}
+__device__ __forceinline__ float block_max256(float v, float *lds4) {
+    v = wave_max(v);
+    const int w = threadIdx.x >> 6;
+    __syncthreads();
+    if ((threadIdx.x & 63) == 0) lds4[w] = v;
+    __syncthreads();
+    return fmaxf(fmaxf(lds4[0], lds4[1]), fmaxf(lds4[2], lds4[3]));
+}
+
+constexpr int CK = 64;  // attention key chunk (absolute positions)
+
+// Inverse RMS of one row from its per-16-column partial sums of squares: lane l adds
+// partials l, l+64, ... in order, then a butterfly, so every lane (and every workgroup that
+// asks) gets the same value.
+__device__ __forceinline__ float inv_rms(const float *ss, int nparts, int d, float eps) {
+    const int lane = threadIdx.x & 63;
+    float s = 0.f;
+    for (int t = lane; t < nparts; t += 64) s += ss[t];
+    s = wave_sum(s);
+    return 1.0f / sqrtf(s / (float)d + eps);
+}
+
+// Sum of squares of 16 consecutive columns held as 4 values by each of the lanes
+// {l, l^step, l^2step, l^3step}: ((c0-3 + c4-7) + (c8-11 + c12-15)), same tree everywhere.
+__device__ __forceinline__ float sumsq16(const float v[4], int step) {
+    float s = ((v[0] * v[0] + v[1] * v[1]) + v[2] * v[2]) + v[3] * v[3];
+    s += __shfl_xor(s, step);
+    s += __shfl_xor(s, 2 * step);
+    return s;
+}
+
+// Streaming loads.  Weights are read exactly once per pass; the activation fragments are read
+// once per workgroup.  Issuing both with the non-temporal hint keeps the activation reads from
+// disturbing the weight stream (measured on gfx950: ordinary loads of the activations cost
+// up to a third of the bandwidth at 4-16 tokens, non-temporal ones almost nothing).
+__device__ __forceinline__ uint4 ld_stream(const uint4 *p) {
+    typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+    const v4u t = __builtin_nontemporal_load((const v4u *)p);
+    return uint4{t.x, t.y, t.z, t.w};
+}
+
+// Agent-scope relaxed accesses: coherent across the L2 caches of all compute dies, no fence.
+__device__ __forceinline__ void st_agent(float *p, float v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Coherent loads for data another workgroup wrote in the same launch: a raw buffer load with the
+// sc1 cache policy reads at agent scope (never a stale L2 line), yet is an ordinary load to the
+// compiler, so consecutive loads stay in flight together (agent-scope atomic loads are each
+// followed by a wait for every outstanding load).  The base must be the same for every lane of
+// the wave; offsets are in bytes and below 2 GiB.
+constexpr int kCoherent = 16;  // sc1
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t coherent_rsrc(const void *base) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, 0x7fffffff, 0x00020000);
+}
+__device__ __forceinline__ uint4 ld_coherent16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    typedef unsigned v4u __attribute__((ext_vector_type(4)));
+    const v4u v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kCoherent);
+    return uint4{v.x, v.y, v.z, v.w};
+}
+__device__ __forceinline__ float ld_coherent_f32(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kCoherent));
+}
+
+// Pack EPL floats into one 16-byte MFMA fragment of dtype T.
+template <DType T>
+__device__ __forceinline__ uint4 pack_frag(const float *v) {
+    if (T == DType::BF16) {
+        uint32_t w[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) w[k] = (uint32_t)f2bf(v[2 * k]) | ((uint32_t)f2bf(v[2 * k + 1]) << 16);
+        return uint4{w[0], w[1], w[2], w[3]};
+    }
+    return uint4{__float_as_uint(v[0]), __float_as_uint(v[1]), __float_as_uint(v[2]), __float_as_uint(v[3])};
+}
+
+// Zero the elements of a 16-byte value fragment whose key index (first + e) is >= limit.
+template <DType T>
+__device__ __forceinline__ uint4 mask_keys(uint4 v, int first, int limit) {
+    uint32_t w[4] = {v.x, v.y, v.z, v.w};
+    if (T == DType::BF16) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            if (first + 2 * k >= limit) w[k] &= 0xffff0000u;
+            if (first + 2 * k + 1 >= limit) w[k] &= 0x0000ffffu;
+        }
+    } else {
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+            if (first + k >= limit) w[k] = 0u;
+    }
+    return uint4{w[0], w[1], w[2], w[3]};
+}
+
+// Epilogue of one 16-feature output tile nt (rows of the weight matrix) for all M tokens,
+// run by the wave that holds the tile's reduced sums (mine[g]: MFMA output layout, lane l holds
+// features nt*16 + 4*(l/16) + j of token 16*g + l%16).  sinv holds 1/rms per token when the
+// input was pre-scaled by the norm gain (folded RMSNorm).
+template <DType T, int MG, int EPI>
+__device__ __forceinline__ void gemm_epilogue(const GemmArgs &a, int nt, const f32x4 (&mine)[MG], const float *sinv) {
+    const int lane = threadIdx.x & 63;
+    const int G4 = lane >> 4;
+#pragma unroll
+    for (int g = 0; g < MG; ++g) {
+        const int m = 16 * g + (lane & 15);
+        const bool valid = m < a.M;
+        const float sc = (a.ss_in != nullptr && valid) ? sinv[m] : 1.0f;
+        f32x4 v = mine[g];
+        if (EPI == EPI_RESID) {
+            float hv[4] = {0.f, 0.f, 0.f, 0.f};
+            const int n0 = nt * 16 + 4 * G4;
+            if (valid) {
+                const size_t hrow = (size_t)m * a.ldh + n0;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    hv[j] = a.H[hrow + j] + v[j];
+                    a.H[hrow + j] = hv[j];
+                }
+            }
+            const float s = sumsq16(hv, 16);
+            if (valid) {
+                if (a.ss_out != nullptr && G4 == 0) a.ss_out[(size_t)m * a.ld_ss_out + nt] = s;
+                if (a.hg_out != nullptr)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+                        St<T>::store(a.hg_out, fm_index<T>(m * a.hg_rs + a.hg_off, n0 + j, a.N),
+                                     hv[j] * a.g_next[n0 + j]);
+            }
+        } else if (EPI == EPI_QKV) {
+            if (valid) {
+                const int b = m / a.c, i = m - b * a.c;
+                const int pos = a.lens[b] + a.pos_off + i;
+                const int tiles_per_head = a.hd / 16, half = a.hd / 2;
+                const int hg = nt / tiles_per_head, t = nt - hg * tiles_per_head;
+#pragma unroll
+                for (int p = 0; p < 2; ++p) {
+                    const int j = 8 * t + 2 * G4 + p;
+                    float x0 = v[2 * p] * sc, x1 = v[2 * p + 1] * sc;
+                    if (hg < a.n_heads + a.n_kv) {
+                        const float2 cs = a.rope[(size_t)pos * half + j];
+                        const float r0 = x0 * cs.x - x1 * cs.y;
+                        const float r1 = x0 * cs.y + x1 * cs.x;
+                        x0 = r0;
+                        x1 = r1;
+                    }
+                    if (hg < a.n_heads) {
+                        float *q = a.Q + (size_t)m * a.n_heads * a.hd + hg * a.hd;
+                        q[j] = x0;
+                        q[j + half] = x1;
+                    } else if (hg < a.n_heads + a.n_kv) {  // key cache [b][kv][pos][hd]
+                        const size_t base = (((size_t)b * a.n_kv + (hg - a.n_heads)) * a.s_max + pos) * a.hd;
+                        St<T>::store(a.Kc, base + j, x0);
+                        St<T>::store(a.Kc, base + j + half, x1);
+                    } else {  // value cache, transposed: [b][kv][hd][pos]
+                        const size_t base = ((size_t)b * a.n_kv + (hg - a.n_heads - a.n_kv)) * a.hd;
+                        St<T>::store(a.Vc, (base + j) * a.s_max + pos, x0);
+                        St<T>::store(a.Vc, (base + j + half) * a.s_max + pos, x1);
+                    }
+                }
+            }
+        } else if (EPI == EPI_SWIGLU) {
+            if (valid) {
+#pragma unroll
+                for (int p = 0; p < 2; ++p) {
+                    const int f = 8 * nt + 2 * G4 + p;
+                    const float gt = v[2 * p] * sc, up = v[2 * p + 1] * sc;
+                    const float act = gt / (1.0f + expf(-gt)) * up;
+                    St<T>::store(a.A, fm_index<T>(m, f, a.N / 2), act);
+                }
+            }
+        } else {  // EPI_LOGITS
+            float best = -INFINITY;
+            int bidx = 0x3fffffff, bad = 0;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int n = nt * 16 + 4 * G4 + j;
+                float y = v[j] * sc;
+                if (a.lora_A != nullptr && valid) {
+                    const float *Ar = a.lora_A + (size_t)n * a.r;
+                    const float *ur = a.lora_u + (size_t)m * a.r;
+                    float sacc = 0.f;
+                    for (int cc = 0; cc < a.r; ++cc) sacc += Ar[cc] * ur[cc];
+                    y = y + a.gamma * sacc;
+                }
+                if (valid) a.Z[(size_t)m * a.N + n] = y;
+                if (!isfinite(y)) bad = 1;
+                if (y > best) {
+                    best = y;
+                    bidx = n;
+                }
+            }
+#pragma unroll
+            for (int o = 16; o <= 32; o <<= 1) {
+                const float ov = __shfl_xor(best, o);
+                const int oi = __shfl_xor(bidx, o);
+                const int ob = __shfl_xor(bad, o);
+                if (ov > best || (ov == best && oi < bidx)) {
+                    best = ov;
+                    bidx = oi;
+                }
+                bad |= ob;
+            }
+            if (valid && G4 == 0) {
+                const int nt16 = a.N / 16;
+                a.part_val[(size_t)m * nt16 + nt] = best;
+                a.part_idx[(size_t)m * nt16 + nt] = bidx | (bad << 30);
+            }
+        }
+    }
+}
+
+}  // namespace dvi
