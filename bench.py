@@ -156,6 +156,9 @@ def main():
             if st["fresh"] > 0:
                 eng.baseline = sched.ema(eng.baseline, st["fresh_accepted"] / st["fresh"])
             eng.updates += 1
+            if stats is not None:
+                stats["update_ms"].append(eng.timings()["update"])
+                stats["update_rows"].append(st["rows"])
         if stats is not None:
             tm = eng.timings()
             stats["tokens"] += int(n.sum())
@@ -177,7 +180,8 @@ def main():
     eng_lens = [P] * B
     for _ in range(W):
         step(k)
-    st = {"tokens": 0, "m": [], "n": [], "verify_ms": [], "draft_ms": [], "verify_bytes": [], "draft_bytes": []}
+    st = {"tokens": 0, "m": [], "n": [], "verify_ms": [], "draft_ms": [], "verify_bytes": [], "draft_bytes": [],
+          "update_ms": [], "update_rows": []}
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(K):
@@ -195,6 +199,21 @@ def main():
     dr_gbs = float(np.mean(st["draft_bytes"])) / (dr_ms * 1e-3) / 1e9
     log("timed %d steps: %.1f tokens/s, %.2f ms/step, mean m %.2f, verify %.3f ms (%.0f GB/s), "
         "draft %.3f ms (%.0f GB/s)" % (K, value, ms_step, mv.mean(), ver_ms, ver_gbs, dr_ms, dr_gbs))
+    # drafter update (the workloads that train the drafter): its dense work is the LoRA head
+    # forward over the ring, rows x V x (d + r) multiply-adds, plus the gradient products
+    upd = None
+    if st["update_ms"]:
+        u_ms = float(np.median(st["update_ms"]))
+        rows = int(np.median(st["update_rows"]))
+        V, d, r = shape.vocab, shape.d_model, shape.lora_rank
+        flops = 2.0 * rows * V * (d + r) + 2.0 * (V * r * rows + rows * V * r + r * d * rows)
+        tfs = flops / (u_ms * 1e-3) / 1e12
+        peak = 2500.0 if shape.bf16 else 157.3
+        upd = {"updates": len(st["update_ms"]), "ms": round(u_ms, 4), "rows": rows, "gflop": round(flops / 1e9, 2),
+               "tflop_s": round(tfs, 2), "mfma_peak_tflop_s": peak, "frac": round(tfs / peak, 4),
+               "head_bytes": shape.vocab * shape.d_model * (2 if shape.bf16 else 4)}
+        log("drafter update: %d updates, median %.3f ms over %d rows: %.1f GFLOP -> %.1f TFLOP/s (%.3f of %g)"
+            % (len(st["update_ms"]), u_ms, rows, flops / 1e9, tfs, tfs / peak, peak))
 
     # dominant kernel: every launch of one kernel class timed with HIP events on the engine's stream
     # (a sequence that has all its tokens keeps computing with its commits masked, so the
@@ -225,7 +244,8 @@ def main():
         eng_lens[:] = [P] * B
         for _ in range(W):
             step(1)
-        sa = {"tokens": 0, "m": [], "n": [], "verify_ms": [], "draft_ms": [], "verify_bytes": [], "draft_bytes": []}
+        sa = {"tokens": 0, "m": [], "n": [], "verify_ms": [], "draft_ms": [], "verify_bytes": [], "draft_bytes": [],
+              "update_ms": [], "update_rows": []}
         KA = min(args.ar_steps, N - 1 - W)
         torch.cuda.synchronize()
         a0 = time.perf_counter()
@@ -280,6 +300,7 @@ def main():
         "acceptance": {"mean_m": round(float(mv.mean()), 4), "mean_tokens_per_step": round(float(nv.mean()), 4),
                        "rate": round(float(mv.mean()) / k, 4)},
         "ar_baseline": ar,
+        "drafter_update": upd,
         "paper_context": PAPER_CONTEXT,
     }
     print(json.dumps(out), flush=True)

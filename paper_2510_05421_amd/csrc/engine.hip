@@ -166,7 +166,7 @@ static size_t layout(dvi_ctx *x, const dvi_config &c, void *base) {
     void *hk_hat = b.take<void>(Bk * d * es);
     void *dfm = b.take<void>(B16 * d * es);
     void *pfm = b.take<void>(B16 * d * es);
-    void *ufm = b.take<void>((size_t)64 * d * es);
+    void *ufm = b.take<void>((size_t)256 * d * es);
     float *vlogits = b.take<float>(M * V * 4);
     float *dlogits = b.take<float>((size_t)c.max_batch * V * 4);
     float *part_val = b.take<float>(M * (V / 16) * 4);

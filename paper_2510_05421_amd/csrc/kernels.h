@@ -153,7 +153,7 @@ struct UpdateArgs {
     float gamma, tau, baseline, c_kl, c_ce, c_pg, c_ent;
     const float *A, *Bm;    // A_s [V][r], B_s [r][d]
     float *u;               // [n][r]
-    void *xfm;              // FM scratch for 64 replay rows
+    void *xfm;              // FM scratch for 256 replay rows
     float *Z;               // [n][V] drafter logits -> overwritten by g = dL/dz
     float *part_val;        // scratch for the logits GEMM epilogue
     int32_t *part_idx;

@@ -746,37 +746,67 @@ __global__ void upd_counts_kernel(const int8_t *r, const int8_t *fresh, int n, f
 }
 
 // Row i: p = softmax(z), q = softmax(l/tau); KL, entropy, log p(a); then overwrite z with
-// g = alpha p (log p - log q - KL) + beta (p - e_a) + eps p (log p + H).
-__global__ void __launch_bounds__(256) upd_rows_kernel(UpdateArgs u, const float *counts) {
-    __shared__ float red[4];
+// g = alpha p (log p - log q - KL) + beta (p - e_a) + eps p (log p + H).  One 1024-thread
+// workgroup per row; the maxima and normalisers come from one pass with a running rescale.
+__device__ __forceinline__ float block_sum1024(float v, float *lds16) {
+    v = wave_sum(v);
+    const int w = threadIdx.x >> 6;
+    __syncthreads();
+    if ((threadIdx.x & 63) == 0) lds16[w] = v;
+    __syncthreads();
+    float s = 0.f;
+#pragma unroll
+    for (int k = 0; k < 16; ++k) s += lds16[k];
+    return s;
+}
+__device__ __forceinline__ float block_max1024(float v, float *lds16) {
+    v = wave_max(v);
+    const int w = threadIdx.x >> 6;
+    __syncthreads();
+    if ((threadIdx.x & 63) == 0) lds16[w] = v;
+    __syncthreads();
+    float s = -INFINITY;
+#pragma unroll
+    for (int k = 0; k < 16; ++k) s = fmaxf(s, lds16[k]);
+    return s;
+}
+
+__global__ void __launch_bounds__(1024) upd_rows_kernel(UpdateArgs u, const float *counts) {
+    __shared__ float red[16];
     const int i = blockIdx.x;
     float *z = u.Z + (size_t)i * u.V;
     const float *lg = u.logits + (size_t)i * u.V;
     const float itau = 1.0f / u.tau;
-    float mz = -INFINITY, mq = -INFINITY;
-    for (int v = threadIdx.x; v < u.V; v += 256) {
-        mz = fmaxf(mz, z[v]);
-        mq = fmaxf(mq, lg[v] * itau);
+    // per-thread running maximum and rescaled sum of both distributions
+    float mz = -INFINITY, mq = -INFINITY, sz = 0.f, sq = 0.f;
+    for (int v = threadIdx.x; v < u.V; v += 1024) {
+        const float a = z[v], b = lg[v] * itau;
+        if (a > mz) {
+            sz = sz * expf(mz - a) + 1.f;
+            mz = a;
+        } else {
+            sz += expf(a - mz);
+        }
+        if (b > mq) {
+            sq = sq * expf(mq - b) + 1.f;
+            mq = b;
+        } else {
+            sq += expf(b - mq);
+        }
     }
-    mz = block_max256(mz, red);
-    mq = block_max256(mq, red);
-    float sz = 0.f, sq = 0.f;
-    for (int v = threadIdx.x; v < u.V; v += 256) {
-        sz += expf(z[v] - mz);
-        sq += expf(lg[v] * itau - mq);
-    }
-    sz = block_sum256(sz, red);
-    sq = block_sum256(sq, red);
-    const float lz = mz + logf(sz), lq = mq + logf(sq);
+    const float Mz = block_max1024(mz, red), Mq = block_max1024(mq, red);
+    sz = block_sum1024(mz == -INFINITY ? 0.f : sz * expf(mz - Mz), red);
+    sq = block_sum1024(mq == -INFINITY ? 0.f : sq * expf(mq - Mq), red);
+    const float lz = Mz + logf(sz), lq = Mq + logf(sq);
     float kl = 0.f, ent = 0.f;
-    for (int v = threadIdx.x; v < u.V; v += 256) {
+    for (int v = threadIdx.x; v < u.V; v += 1024) {
         const float lp = z[v] - lz, lqv = lg[v] * itau - lq;
         const float p = expf(lp);
         kl += p * (lp - lqv);
         ent -= p * lp;
     }
-    kl = block_sum256(kl, red);
-    ent = block_sum256(ent, red);
+    kl = block_sum1024(kl, red);
+    ent = block_sum1024(ent, red);
     const int ai = u.a[i];
     const float lpa = z[ai] - lz;
     const float n = counts[0], na = counts[1], nf = counts[2];
@@ -784,8 +814,8 @@ __global__ void __launch_bounds__(256) upd_rows_kernel(UpdateArgs u, const float
     const float alpha = u.c_kl / n;
     const float beta = u.c_ce * ri / fmaxf(na, 1.f) + u.c_pg * (ri - u.baseline) * fi / fmaxf(nf, 1.f);
     const float eps = u.c_ent / n;
-    __syncthreads();
-    for (int v = threadIdx.x; v < u.V; v += 256) {
+    __syncthreads();  // every thread has read z[ai] before it is overwritten
+    for (int v = threadIdx.x; v < u.V; v += 1024) {
         const float lp = z[v] - lz, lqv = lg[v] * itau - lq;
         const float p = expf(lp);
         const float g = alpha * p * (lp - lqv - kl) + beta * (p - (v == ai ? 1.f : 0.f)) + eps * p * (lp + ent);
@@ -822,80 +852,206 @@ __global__ void upd_loss_kernel(UpdateArgs u, const float *counts) {
     u.loss_out[8] = counts[3];
 }
 
-// dA[v][c] = gamma * sum_i g[i][v] u[i][c]   (one thread per vocabulary row v)
+// The LoRA gradients run with a fixed 64-slot accumulator per thread (rank <= 64), fully
+// unrolled and guarded by the rank so the slots stay in registers.
+constexpr int kMaxRank = 64;
+
+// dA[v][c] = gamma * sum_i g[i][v] u[i][c]   (one thread per vocabulary row v; rows i in order).
+// The workgroup stages u for up to 256 rows in LDS and walks the rows in blocks of that size.
 __global__ void __launch_bounds__(256) upd_dA_kernel(UpdateArgs u) {
+    __shared__ float us[256 * kMaxRank];
     const int v = blockIdx.x * 256 + threadIdx.x;
-    if (v >= u.V) return;
-    float acc[64];
-    for (int c = 0; c < u.rank; ++c) acc[c] = 0.f;
-    for (int i = 0; i < u.n; ++i) {
-        const float g = u.Z[(size_t)i * u.V + v];
-        for (int c = 0; c < u.rank; ++c) acc[c] += g * u.u[(size_t)i * u.rank + c];
+    float acc[kMaxRank];
+#pragma unroll
+    for (int c = 0; c < kMaxRank; ++c) acc[c] = 0.f;
+    for (int i0 = 0; i0 < u.n; i0 += 256) {
+        const int ni = min(256, u.n - i0);
+        __syncthreads();
+        for (int e = threadIdx.x; e < ni * u.rank; e += 256) us[e] = u.u[(size_t)i0 * u.rank + e];
+        __syncthreads();
+        if (v < u.V) {
+#pragma unroll 4
+            for (int i = 0; i < ni; ++i) {
+                const float g = u.Z[(size_t)(i0 + i) * u.V + v];
+#pragma unroll
+                for (int c = 0; c < kMaxRank; ++c)
+                    if (c < u.rank) acc[c] += g * us[i * u.rank + c];
+            }
+        }
     }
-    for (int c = 0; c < u.rank; ++c) u.dA[(size_t)v * u.rank + c] = u.gamma * acc[c];
+    if (v < u.V)
+#pragma unroll
+        for (int c = 0; c < kMaxRank; ++c)
+            if (c < u.rank) u.dA[(size_t)v * u.rank + c] = u.gamma * acc[c];
 }
 
-// du[i][c] = gamma * sum_v A[v][c] g[i][v]   (one workgroup per row i)
-__global__ void __launch_bounds__(256) upd_du_kernel(UpdateArgs u) {
-    __shared__ float red[4];
-    const int i = blockIdx.x;
-    for (int c = 0; c < u.rank; ++c) {
+// du[i][c] = gamma * sum_v A[v][c] g[i][v]   (one 512-thread workgroup per row i).  Thread t
+// takes v = t, t+512, ... in order, reading whole rows of A (16-byte loads), and the 512 partial
+// vectors are summed in a fixed tree (butterfly per wave, then the waves in order).
+__global__ void __launch_bounds__(512) upd_du_kernel(UpdateArgs u) {
+    __shared__ float part[8][kMaxRank + 1];
+    const int i = blockIdx.x, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    float acc[kMaxRank];
+#pragma unroll
+    for (int c = 0; c < kMaxRank; ++c) acc[c] = 0.f;
+    const float *g = u.Z + (size_t)i * u.V;
+    const bool vec = (u.rank & 3) == 0;
+#pragma unroll 4
+    for (int v = threadIdx.x; v < u.V; v += 512) {
+        const float gv = g[v];
+        const float *Av = u.A + (size_t)v * u.rank;
+        if (vec) {
+#pragma unroll
+            for (int c4 = 0; c4 < kMaxRank / 4; ++c4)
+                if (4 * c4 < u.rank) {
+                    const float4 a4 = ((const float4 *)Av)[c4];
+                    acc[4 * c4 + 0] += a4.x * gv;
+                    acc[4 * c4 + 1] += a4.y * gv;
+                    acc[4 * c4 + 2] += a4.z * gv;
+                    acc[4 * c4 + 3] += a4.w * gv;
+                }
+        } else {
+#pragma unroll
+            for (int c = 0; c < kMaxRank; ++c)
+                if (c < u.rank) acc[c] += Av[c] * gv;
+        }
+    }
+    // fixed tree: butterfly inside each wave, then the 8 wave sums in order
+#pragma unroll
+    for (int c = 0; c < kMaxRank; ++c)
+        if (c < u.rank) {
+            const float sw = wave_sum(acc[c]);
+            if (lane == 0) part[w][c] = sw;
+        }
+    __syncthreads();
+    if (threadIdx.x < u.rank) {
         float s = 0.f;
-        for (int v = threadIdx.x; v < u.V; v += 256) s += u.A[(size_t)v * u.rank + c] * u.Z[(size_t)i * u.V + v];
-        s = block_sum256(s, red);
-        if (threadIdx.x == 0) u.du[(size_t)i * u.rank + c] = u.gamma * s;
+        for (int t = 0; t < 8; ++t) s += part[t][threadIdx.x];
+        u.du[(size_t)i * u.rank + threadIdx.x] = u.gamma * s;
     }
 }
 
-// dB[c][k] = sum_i du[i][c] h[i][k]   (one thread per model dim k)
+// dB[c][k] = sum_i du[i][c] h[i][k]   (one thread per (k, c); rows i in order)
 template <DType T>
 __global__ void __launch_bounds__(256) upd_dB_kernel(UpdateArgs u) {
-    const int k = blockIdx.x * 256 + threadIdx.x;
+    const int k = blockIdx.x * 256 + threadIdx.x, c = blockIdx.y;
     if (k >= u.d) return;
-    float acc[64];
-    for (int c = 0; c < u.rank; ++c) acc[c] = 0.f;
-    for (int i = 0; i < u.n; ++i) {
-        const float hv = St<T>::load(u.Hh, (size_t)i * u.d + k);
-        for (int c = 0; c < u.rank; ++c) acc[c] += u.du[(size_t)i * u.rank + c] * hv;
+    float acc = 0.f;
+#pragma unroll 4
+    for (int i = 0; i < u.n; ++i) acc += u.du[(size_t)i * u.rank + c] * St<T>::load(u.Hh, (size_t)i * u.d + k);
+    u.dB[(size_t)c * u.d + k] = acc;
+}
+
+// Drafter logits of the replay rows on MFMA: Z[m][v] = X[m] . W[v] + gamma * sum_c A[v][c] u[m][c]
+// for up to 256 rows m (X fragment-major, up to 16 groups of 16).  A workgroup owns a band of 8
+// weight tiles (128 vocabulary rows); wave w takes tiles 2w and 2w+1 for every row group, so the
+// weights leave HBM once and each activation fragment, read by all four waves of the compute
+// unit, mostly hits L1.  Steps are software-pipelined two deep; fragments past the band or the
+// rows load a valid address and enter as zeros, so every MFMA runs unconditionally (MFMA does
+// not honour the EXEC mask).  kUpdG row groups per launch (4, 8 or 16, the rows rounded up),
+// kUpdU steps in flight (deeper when the groups are fewer).
+constexpr int kUpdBand = 8, kUpdTW = 2;
+template <DType T, int kUpdG, int kUpdU>
+__global__ void __launch_bounds__(256) upd_gemm_kernel(const void *W, const void *X, int n, int V, int K,
+                                                       const float *A, const float *uu, int r, float gamma,
+                                                       float *Z) {
+    constexpr int KC = (T == DType::BF16) ? 32 : 16;
+    const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int KT = K / KC, NT = V / 16;
+    const int t0 = blockIdx.x * kUpdBand + kUpdTW * wave;
+    const int ng = (n + 15) / 16;
+    const uint4 zero = {0u, 0u, 0u, 0u};
+    const uint4 *wp = (const uint4 *)W + lane, *xp = (const uint4 *)X + lane;
+    f32x4 acc[kUpdTW][kUpdG];
+#pragma unroll
+    for (int t = 0; t < kUpdTW; ++t)
+#pragma unroll
+        for (int g = 0; g < kUpdG; ++g) acc[t][g] = (f32x4){0.f, 0.f, 0.f, 0.f};
+    uint4 wf[kUpdU][kUpdTW], xf[kUpdU][kUpdG];
+    auto fetch = [&](int slot, int k) {
+        const int kc = min(k, KT - 1);
+#pragma unroll
+        for (int t = 0; t < kUpdTW; ++t) {
+            const int tt = min(t0 + t, NT - 1);
+            const uint4 w = wp[((size_t)tt * KT + kc) * 64];
+            wf[slot][t] = (k < KT && t0 + t < NT) ? w : zero;
+        }
+#pragma unroll
+        for (int g = 0; g < kUpdG; ++g) {
+            const int gg = min(g, ng - 1);
+            const uint4 x = xp[((size_t)gg * KT + kc) * 64];
+            xf[slot][g] = (k < KT && g < ng) ? x : zero;
+        }
+    };
+#pragma unroll
+    for (int s = 0; s < kUpdU; ++s) fetch(s, s);
+    for (int k0 = 0; k0 < KT; k0 += kUpdU) {
+#pragma unroll
+        for (int s = 0; s < kUpdU; ++s) {
+#pragma unroll
+            for (int t = 0; t < kUpdTW; ++t)
+#pragma unroll
+                for (int g = 0; g < kUpdG; ++g) acc[t][g] = St<T>::mma(wf[s][t], xf[s][g], acc[t][g]);
+            fetch(s, k0 + s + kUpdU);
+        }
     }
-    for (int c = 0; c < u.rank; ++c) u.dB[(size_t)c * u.d + k] = acc[c];
+    const int G4 = lane >> 4;
+#pragma unroll
+    for (int t = 0; t < kUpdTW; ++t) {
+        if (t0 + t >= NT) break;
+#pragma unroll
+        for (int g = 0; g < kUpdG; ++g) {
+            const int m = 16 * g + (lane & 15);
+            if (m >= n) continue;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int v = (t0 + t) * 16 + 4 * G4 + j;
+                const float *Av = A + (size_t)v * r, *um = uu + (size_t)m * r;
+                float sl = 0.f;
+                for (int c = 0; c < r; ++c) sl += Av[c] * um[c];
+                Z[(size_t)m * V + v] = acc[t][g][j] + gamma * sl;
+            }
+        }
+    }
 }
 
 void launch_update_forward(DType t, const UpdateArgs &u, hipStream_t s) {
     float *counts = u.loss_out + 12;
     upd_counts_kernel<<<1, 64, 0, s>>>(u.r, u.fresh, u.n, counts);
     launch_lora_u(t, u.Hh, u.Bm, u.n, u.d, u.rank, u.u, s);
-    const size_t es = dtype_size(t);
-    for (int r0 = 0; r0 < u.n; r0 += 64) {
-        const int rows = min(64, u.n - r0);
+    const int bands = (u.V / 16 + kUpdBand - 1) / kUpdBand;
+    for (int r0 = 0; r0 < u.n; r0 += 256) {
+        const int rows = min(256, u.n - r0);
         launch_gather_fm(t, u.Hh, false, 1, r0, rows, u.d, u.xfm, s);
-        GemmArgs g{};
-        g.W = u.W;
-        g.X = u.xfm;
-        g.M = rows;
-        g.N = u.V;
-        g.K = u.d;
-        g.Z = u.Z + (size_t)r0 * u.V;
-        g.lora_A = u.A;
-        g.lora_u = u.u + (size_t)r0 * u.rank;
-        g.r = u.rank;
-        g.gamma = u.gamma;
-        g.part_val = u.part_val;
-        g.part_idx = u.part_idx;
-        launch_gemm(t, EPI_LOGITS, g, s);
+        const float *ur = u.u + (size_t)r0 * u.rank;
+        float *Zr = u.Z + (size_t)r0 * u.V;
+        if (t == DType::BF16) {
+            if (rows <= 64)
+                upd_gemm_kernel<DType::BF16, 4, 4><<<bands, 256, 0, s>>>(u.W, u.xfm, rows, u.V, u.d, u.A, ur, u.rank, u.gamma, Zr);
+            else if (rows <= 128)
+                upd_gemm_kernel<DType::BF16, 8, 3><<<bands, 256, 0, s>>>(u.W, u.xfm, rows, u.V, u.d, u.A, ur, u.rank, u.gamma, Zr);
+            else
+                upd_gemm_kernel<DType::BF16, 16, 2><<<bands, 256, 0, s>>>(u.W, u.xfm, rows, u.V, u.d, u.A, ur, u.rank, u.gamma, Zr);
+        } else {
+            if (rows <= 64)
+                upd_gemm_kernel<DType::F32, 4, 4><<<bands, 256, 0, s>>>(u.W, u.xfm, rows, u.V, u.d, u.A, ur, u.rank, u.gamma, Zr);
+            else if (rows <= 128)
+                upd_gemm_kernel<DType::F32, 8, 3><<<bands, 256, 0, s>>>(u.W, u.xfm, rows, u.V, u.d, u.A, ur, u.rank, u.gamma, Zr);
+            else
+                upd_gemm_kernel<DType::F32, 16, 2><<<bands, 256, 0, s>>>(u.W, u.xfm, rows, u.V, u.d, u.A, ur, u.rank, u.gamma, Zr);
+        }
     }
-    upd_rows_kernel<<<u.n, 256, 0, s>>>(u, counts);
+    upd_rows_kernel<<<u.n, 1024, 0, s>>>(u, counts);
     upd_loss_kernel<<<1, 64, 0, s>>>(u, counts);
 }
 
 void launch_update_backward(DType t, const UpdateArgs &u, hipStream_t s) {
-    (void)t;
     upd_dA_kernel<<<(u.V + 255) / 256, 256, 0, s>>>(u);
-    upd_du_kernel<<<u.n, 256, 0, s>>>(u);
+    upd_du_kernel<<<u.n, 512, 0, s>>>(u);
     if (t == DType::BF16)
-        upd_dB_kernel<DType::BF16><<<(u.d + 255) / 256, 256, 0, s>>>(u);
+        upd_dB_kernel<DType::BF16><<<dim3((u.d + 255) / 256, u.rank), 256, 0, s>>>(u);
     else
-        upd_dB_kernel<DType::F32><<<(u.d + 255) / 256, 256, 0, s>>>(u);
+        upd_dB_kernel<DType::F32><<<dim3((u.d + 255) / 256, u.rank), 256, 0, s>>>(u);
 }
 
 __global__ void adam_kernel(float *p, const float *g, float *m, float *v, int n, float lr, float b1, float b2, float eps,

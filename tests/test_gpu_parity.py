@@ -167,10 +167,12 @@ def test_buffer_rows_hold_the_verify_logits_and_normed_states():
     eng.close()
 
 
-@pytest.mark.parametrize("name,n_rows", [("tiny", 48), ("1b_L4", 200)])
+@pytest.mark.parametrize("name,n_rows", [("tiny", 48), ("tiny", 100), ("tiny", 300), ("1b_L4", 200), ("1b_L4", 256)])
 def test_drafter_update_gradients_match_oracle(name, n_rows):
+    """Row counts cover the update GEMM's 4-, 8- and 16-group variants and more rows than one
+    launch takes (300 > 256)."""
     shape = gu.SHAPES[name]
-    eng, w = gu.engine(shape, max_seq=64, lora_A_std=0.02)
+    eng, w = gu.engine(shape, max_seq=64, lora_A_std=0.02, buffer_rows=max(256, n_rows))
     buf = synth.make_buffer(shape.d_model, shape.vocab, n_rows, seed=11)
     eng.prefill(synth.make_prompts(shape.vocab, 1, 8, 1))
     eng.write_buffer(buf.h, buf.a, buf.logits, buf.r, buf.fresh)
