@@ -18,7 +18,10 @@
  *  - Matrices are row-major [out_features][in_features]; bf16 arrays hold
  *    IEEE bfloat16 bit patterns, fp32 arrays IEEE float.
  *  - All work is enqueued on the stream given to dvi_create.  Calls that return
- *    host data synchronise that stream before returning.
+ *    host data synchronise that stream before returning.  On a stream other
+ *    than the null stream, the kernels of each draft and verify call are
+ *    captured once into a HIP graph per shape (batch, k_spec, variant,
+ *    attention grid bucket) and replayed (see dvi_set_graphs).
  *  - Errors: a negative dvi_status; dvi_last_error() describes the last one.
  *    DVI_ERR_ARG, DVI_ERR_STATE and DVI_ERR_CAPACITY are detected on the host
  *    before anything is launched and leave the context unchanged.
@@ -256,6 +259,20 @@ enum {
 };
 dvi_status dvi_probe_kernel(dvi_ctx *ctx, int32_t which);
 dvi_status dvi_probe_read(dvi_ctx *ctx, double *total_ms, int64_t *launches, double *bytes);
+
+/*
+ * Graph replay of the decode passes (DVI's step structure, Section 3.3: a draft of
+ * k_spec shallow passes and one block verify).  enable = 1 (the default on a
+ * non-null stream): dvi_draft and dvi_verify launch one captured HIP graph per
+ * call, keyed by (batch, k_spec, variant, attention grid bucket); sequence lengths
+ * are read on the device, so a graph stays valid as they grow, and a pass is
+ * captured again only when the longest sequence enters a new 256-position bucket.
+ * Results are bitwise the same as with enable = 0 (every kernel launched
+ * directly).  Disabling frees the cached graphs.  Errors: DVI_ERR_ARG when
+ * enabling on the null stream (which cannot be captured).  While a timing probe
+ * is set, launches are direct.
+ */
+dvi_status dvi_set_graphs(dvi_ctx *ctx, int32_t enable);
 
 /* Per-phase device time of the last call of each kind (ms, hipEvent based). */
 dvi_status dvi_get_timings(dvi_ctx *ctx, double *ms_draft, double *ms_verify, double *ms_commit, double *ms_update);

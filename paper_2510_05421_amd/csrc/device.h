@@ -99,6 +99,19 @@ __device__ __forceinline__ float inv_rms(const float *ss, int nparts, int d, flo
     return 1.0f / sqrtf(s / (float)d + eps);
 }
 
+// inv_rms with the partial sums already in registers: v[k] holds ss[lane + 64k] (k < KP,
+// nparts <= 64*KP); same summation order as inv_rms.
+template <int KP>
+__device__ __forceinline__ float inv_rms_regs(const float (&v)[KP], int nparts, int d, float eps) {
+    const int lane = threadIdx.x & 63;
+    float s = 0.f;
+#pragma unroll
+    for (int k = 0; k < KP; ++k)
+        if (lane + 64 * k < nparts) s += v[k];
+    s = wave_sum(s);
+    return 1.0f / sqrtf(s / (float)d + eps);
+}
+
 // Sum of squares of 16 consecutive columns held as 4 values by each of the lanes
 // {l, l^step, l^2step, l^3step}: ((c0-3 + c4-7) + (c8-11 + c12-15)), same tree everywhere.
 __device__ __forceinline__ float sumsq16(const float v[4], int step) {
@@ -140,6 +153,11 @@ __device__ __forceinline__ uint4 ld_coherent16(__amdgpu_buffer_rsrc_t r, uint32_
 __device__ __forceinline__ float ld_coherent_f32(__amdgpu_buffer_rsrc_t r, uint32_t off) {
     return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kCoherent));
 }
+__device__ __forceinline__ float2 ld_coherent_f32x2(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    typedef unsigned v2u __attribute__((ext_vector_type(2)));
+    const v2u v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, kCoherent);
+    return float2{__uint_as_float(v.x), __uint_as_float(v.y)};
+}
 
 // Pack EPL floats into one 16-byte MFMA fragment of dtype T.
 template <DType T>
@@ -171,12 +189,71 @@ __device__ __forceinline__ uint4 mask_keys(uint4 v, int first, int limit) {
     return uint4{w[0], w[1], w[2], w[3]};
 }
 
+// Operands of a tile's epilogue that do not depend on the product (residual rows and the next
+// norm's gain; positions and rotary (cos, sin)).  The epilogue wave requests them before the
+// weight stream, so the epilogue after it only computes and stores.  Same lane layout as the
+// epilogue: lane l, token 16*g + l%16, features nt*16 + 4*(l/16) + j.
+template <int MG>
+struct EpiOperands {
+    float v[MG][4];  // RESID: H row values; QKV: (cos, sin) of the lane's two rotary pairs
+    float g[4];      // RESID: g_next
+    int pos[MG];     // QKV: position of the token
+};
+
+// Stage 1: everything but the rotary table, whose address needs the position.
+template <int MG, int EPI>
+__device__ __forceinline__ void epilogue_prefetch(const GemmArgs &a, int nt, EpiOperands<MG> &e) {
+    const int lane = threadIdx.x & 63;
+    const int G4 = lane >> 4;
+#pragma unroll
+    for (int g = 0; g < MG; ++g) {
+        const int m = 16 * g + (lane & 15);
+        const int row = m < a.M ? m : 0;  // rows past M read row 0 and are never used
+        if (EPI == EPI_RESID) {
+            const float4 h4 = *(const float4 *)(a.H + (size_t)row * a.ldh + nt * 16 + 4 * G4);
+            e.v[g][0] = h4.x;
+            e.v[g][1] = h4.y;
+            e.v[g][2] = h4.z;
+            e.v[g][3] = h4.w;
+        } else if (EPI == EPI_QKV) {
+            const int b = row / a.c, i = row - b * a.c;
+            e.pos[g] = a.lens[b] + a.pos_off + i;
+        }
+    }
+    if (EPI == EPI_RESID && a.hg_out != nullptr) {
+        const float4 g4 = *(const float4 *)(a.g_next + nt * 16 + 4 * G4);
+        e.g[0] = g4.x;
+        e.g[1] = g4.y;
+        e.g[2] = g4.z;
+        e.g[3] = g4.w;
+    }
+}
+
+// Stage 2: rotary (cos, sin) at the positions of stage 1.
+template <int MG, int EPI>
+__device__ __forceinline__ void epilogue_prefetch_rope(const GemmArgs &a, int nt, EpiOperands<MG> &e) {
+    if (EPI != EPI_QKV) return;
+    const int G4 = (threadIdx.x & 63) >> 4;
+    const int tiles_per_head = a.hd / 16, half = a.hd / 2;
+    const int hg = nt / tiles_per_head, t = nt - hg * tiles_per_head;
+    if (hg >= a.n_heads + a.n_kv) return;  // values are not rotated
+#pragma unroll
+    for (int g = 0; g < MG; ++g)
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+            const float2 cs = a.rope[(size_t)e.pos[g] * half + 8 * t + 2 * G4 + p];
+            e.v[g][2 * p] = cs.x;
+            e.v[g][2 * p + 1] = cs.y;
+        }
+}
+
 // Epilogue of one 16-feature output tile nt (rows of the weight matrix) for all M tokens,
 // run by the wave that holds the tile's reduced sums (mine[g]: MFMA output layout, lane l holds
-// features nt*16 + 4*(l/16) + j of token 16*g + l%16).  sinv holds 1/rms per token when the
-// input was pre-scaled by the norm gain (folded RMSNorm).
+// features nt*16 + 4*(l/16) + j of token 16*g + l%16) and the tile's prefetched operands e.
+// sinv holds 1/rms per token when the input was pre-scaled by the norm gain (folded RMSNorm).
 template <DType T, int MG, int EPI>
-__device__ __forceinline__ void gemm_epilogue(const GemmArgs &a, int nt, const f32x4 (&mine)[MG], const float *sinv) {
+__device__ __forceinline__ void gemm_epilogue(const GemmArgs &a, int nt, const f32x4 (&mine)[MG], const float *sinv,
+                                              const EpiOperands<MG> &e) {
     const int lane = threadIdx.x & 63;
     const int G4 = lane >> 4;
 #pragma unroll
@@ -192,7 +269,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &a, int nt, const f
                 const size_t hrow = (size_t)m * a.ldh + n0;
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
-                    hv[j] = a.H[hrow + j] + v[j];
+                    hv[j] = e.v[g][j] + v[j];
                     a.H[hrow + j] = hv[j];
                 }
             }
@@ -202,13 +279,12 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &a, int nt, const f
                 if (a.hg_out != nullptr)
 #pragma unroll
                     for (int j = 0; j < 4; ++j)
-                        St<T>::store(a.hg_out, fm_index<T>(m * a.hg_rs + a.hg_off, n0 + j, a.N),
-                                     hv[j] * a.g_next[n0 + j]);
+                        St<T>::store(a.hg_out, fm_index<T>(m * a.hg_rs + a.hg_off, n0 + j, a.N), hv[j] * e.g[j]);
             }
         } else if (EPI == EPI_QKV) {
             if (valid) {
-                const int b = m / a.c, i = m - b * a.c;
-                const int pos = a.lens[b] + a.pos_off + i;
+                const int b = m / a.c;
+                const int pos = e.pos[g];
                 const int tiles_per_head = a.hd / 16, half = a.hd / 2;
                 const int hg = nt / tiles_per_head, t = nt - hg * tiles_per_head;
 #pragma unroll
@@ -216,7 +292,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &a, int nt, const f
                     const int j = 8 * t + 2 * G4 + p;
                     float x0 = v[2 * p] * sc, x1 = v[2 * p + 1] * sc;
                     if (hg < a.n_heads + a.n_kv) {
-                        const float2 cs = a.rope[(size_t)pos * half + j];
+                        const float2 cs = {e.v[g][2 * p], e.v[g][2 * p + 1]};
                         const float r0 = x0 * cs.x - x1 * cs.y;
                         const float r1 = x0 * cs.y + x1 * cs.x;
                         x0 = r0;
@@ -230,10 +306,11 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &a, int nt, const f
                         const size_t base = (((size_t)b * a.n_kv + (hg - a.n_heads)) * a.s_max + pos) * a.hd;
                         St<T>::store(a.Kc, base + j, x0);
                         St<T>::store(a.Kc, base + j + half, x1);
-                    } else {  // value cache, transposed: [b][kv][hd][pos]
-                        const size_t base = ((size_t)b * a.n_kv + (hg - a.n_heads - a.n_kv)) * a.hd;
-                        St<T>::store(a.Vc, (base + j) * a.s_max + pos, x0);
-                        St<T>::store(a.Vc, (base + j + half) * a.s_max + pos, x1);
+                    } else {  // value cache, chunk-major: [b][kv][pos / 64][hd][pos % 64]
+                        const size_t base = ((size_t)b * a.n_kv + (hg - a.n_heads - a.n_kv)) * a.hd * a.s_max +
+                                            (size_t)(pos / CK) * a.hd * CK + pos % CK;
+                        St<T>::store(a.Vc, base + (size_t)j * CK, x0);
+                        St<T>::store(a.Vc, base + (size_t)(j + half) * CK, x1);
                     }
                 }
             }

@@ -9,6 +9,8 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <array>
+#include <map>
 #include <vector>
 
 #include "../../include/dvi.h"
@@ -87,6 +89,9 @@ struct dvi_ctx {
     bool ev_ok = false;
     float ms[4] = {0, 0, 0, 0};
     int ev_pending[4] = {0, 0, 0, 0};
+    // captured decode passes: (phase, B, k_spec, variant, attention chunks) -> graph
+    bool graphs = false;
+    std::map<std::array<int, 5>, hipGraphExec_t> gcache;
     // kernel probe
     int probe = 0;
     std::vector<hipEvent_t> pev;
@@ -296,6 +301,7 @@ extern "C" dvi_status dvi_create(const dvi_config *cfg, const dvi_weights *w, vo
     x->es = dtype_size(x->dt);
     x->s_cap = cache_cap(*cfg);
     x->stream = (hipStream_t)stream;
+    x->graphs = stream != nullptr;
     layout(x, *cfg, ws);
     x->lora_A = w->lora_A;
     x->lora_B = w->lora_B;
@@ -395,8 +401,14 @@ extern "C" dvi_status dvi_create(const dvi_config *cfg, const dvi_weights *w, vo
     return DVI_OK;
 }
 
+static void drop_graphs(dvi_ctx *x) {
+    for (auto &kv : x->gcache) (void)hipGraphExecDestroy(kv.second);
+    x->gcache.clear();
+}
+
 extern "C" void dvi_destroy(dvi_ctx *x) {
     if (!x) return;
+    drop_graphs(x);
     if (x->ev_ok)
         for (int i = 0; i < 8; ++i) (void)hipEventDestroy(x->ev[i]);
     for (auto &e : x->pev) (void)hipEventDestroy(e);
@@ -461,17 +473,26 @@ static const float *next_gain(dvi_ctx *x, int l) {
     return l + 1 < x->cfg.n_layers ? x->L[l + 1].attn_norm : x->final_norm;
 }
 
-static dvi_status run_layers(dvi_ctx *x, int l0, int l1, int B, int c, int pos_off, float *h, float *ss, void *hg,
-                             int rs, void *out_hg, int out_rs, int out_off) {
+// Attention grid of a call whose rows reach at most position pmax: its 64-key chunks rounded up
+// to a multiple of 4 (a 256-position bucket), so that a captured pass stays valid until the
+// longest sequence crosses a bucket edge.  Workgroups past a sequence's own chunks exit at once.
+static int attn_chunks(const dvi_ctx *x, int pmax) {
+    const int n = (pmax / 64 + 1 + 3) / 4 * 4;
+    return n < x->chunk_stride ? n : x->chunk_stride;
+}
+
+static int max_len(const dvi_ctx *x) {
+    int m = 0;
+    for (int b = 0; b < x->B; ++b) m = x->lens_h[b] > m ? x->lens_h[b] : m;
+    return m;
+}
+
+static dvi_status run_layers(dvi_ctx *x, int l0, int l1, int B, int c, int pos_off, int n_chunks, float *h, float *ss,
+                             void *hg, int rs, void *out_hg, int out_rs, int out_off) {
     const dvi_config &cf = x->cfg;
     const int d = cf.d_model, F = cf.ffn_dim, H = cf.n_heads, Hkv = cf.n_kv_heads, hd = cf.head_dim;
     const int nps = d / 16;
     const int M = B * c;
-    int pmax = 0;
-    for (int b = 0; b < B; ++b) {
-        const int p = x->lens_h[b] + pos_off + c - 1;
-        if (p > pmax) pmax = p;
-    }
     for (int l = l0; l < l1; ++l) {
         const LayerW &Lw = x->L[l];
         GemmArgs a{};
@@ -494,7 +515,7 @@ static dvi_status run_layers(dvi_ctx *x, int l0, int l1, int B, int c, int pos_o
         at.Q = x->q;
         at.Kc = Lw.Kc;
         at.Vc = Lw.Vc;
-        for (int b = 0; b < B; ++b) at.len[b] = x->lens_h[b];
+        at.lens = x->lens;
         at.B = B;
         at.c = c;
         at.pos_off = pos_off;
@@ -503,7 +524,7 @@ static dvi_status run_layers(dvi_ctx *x, int l0, int l1, int B, int c, int pos_o
         at.hd = hd;
         at.s_max = x->s_cap;
         at.scale = 1.0f / sqrtf((float)hd);
-        at.n_chunks = pmax / 64 + 1;
+        at.n_chunks = n_chunks;
         at.chunk_stride = x->chunk_stride;
         at.part_o = x->att_po;
         at.part_ml = x->att_pml;
@@ -584,6 +605,43 @@ static void ev_end(dvi_ctx *x, int phase) {
     }
 }
 
+// Runs body (a sequence of kernel launches on the context's stream) directly, or as the captured
+// graph of key, capturing it on first use.  A failed capture leaves nothing cached.
+constexpr size_t kMaxGraphs = 64;
+
+template <typename Body>
+static dvi_status run_pass(dvi_ctx *x, const std::array<int, 5> &key, Body &&body) {
+    if (!x->graphs || x->probe != DVI_PROBE_OFF) return body();
+    auto it = x->gcache.find(key);
+    if (it == x->gcache.end()) {
+        if (x->gcache.size() >= kMaxGraphs) drop_graphs(x);
+        HIPCHK(x, hipStreamBeginCapture(x->stream, hipStreamCaptureModeThreadLocal));
+        const dvi_status st = body();
+        hipGraph_t g = nullptr;
+        const hipError_t e = hipStreamEndCapture(x->stream, &g);
+        if (st != DVI_OK) {
+            if (g) (void)hipGraphDestroy(g);
+            return st;
+        }
+        if (e != hipSuccess) return fail(x, DVI_ERR_DEVICE, "hipStreamEndCapture: %s", hipGetErrorString(e));
+        hipGraphExec_t ge = nullptr;
+        const hipError_t ei = hipGraphInstantiate(&ge, g, nullptr, nullptr, 0);
+        (void)hipGraphDestroy(g);
+        if (ei != hipSuccess) return fail(x, DVI_ERR_DEVICE, "hipGraphInstantiate: %s", hipGetErrorString(ei));
+        it = x->gcache.emplace(key, ge).first;
+    }
+    HIPCHK(x, hipGraphLaunch(it->second, x->stream));
+    return DVI_OK;
+}
+
+extern "C" dvi_status dvi_set_graphs(dvi_ctx *x, int32_t enable) {
+    if (!x) return DVI_ERR_ARG;
+    if (enable && x->stream == nullptr) return fail(x, DVI_ERR_ARG, "graphs need a stream other than the null stream");
+    if (!enable) drop_graphs(x);
+    x->graphs = enable != 0;
+    return DVI_OK;
+}
+
 // ------------------------------------------------------------------------------------------
 // C ABI: decode step
 // ------------------------------------------------------------------------------------------
@@ -620,7 +678,8 @@ extern "C" dvi_status dvi_prefill(dvi_ctx *x, int32_t batch, const int32_t *ids,
         const int cc = (P - s0) < c ? P - s0 : c;
         launch_embed(x->dt, x->emb, x->ids + s0, P, batch, cc, d, x->h, d, x->ss, nps, x->hg, x->L[0].attn_norm,
                      x->stream);
-        dvi_status st = run_layers(x, 0, cf.n_layers, batch, cc, s0, x->h, x->ss, x->hg, 1, x->hg, 1, 0);
+        dvi_status st =
+            run_layers(x, 0, cf.n_layers, batch, cc, s0, attn_chunks(x, s0 + cc - 1), x->h, x->ss, x->hg, 1, x->hg, 1, 0);
         if (st != DVI_OK) return st;
         if (s0 + cc == P) {  // last prompt token of every sequence -> first generated token
             launch_gather_fm(x->dt, x->hg, true, cc, cc - 1, batch, d, x->pfm, x->stream);
@@ -663,23 +722,30 @@ extern "C" dvi_status dvi_draft(dvi_ctx *x, int32_t k_spec, const int32_t *force
     HIPCHK(x, hipMemsetAsync(flags_ptr(x), 0, 16, x->stream));
     x->ar_mode = (k_spec == 1 && !forced) ? 1 : 0;
     const int nps = d / 16;
-    for (int j = 0; j < k_spec; ++j) {
-        // draft token j of sequence b lives in row b*k_spec + j of hk / hk_ss / hk_hg
-        const int32_t *tok = j == 0 ? x->pending : x->drafts + (j - 1);
-        float *h = x->hk + (size_t)j * d;
-        float *ss = x->hk_ss + (size_t)j * nps;
-        launch_embed(x->dt, x->emb, tok, j == 0 ? 1 : k_spec, B, 1, d, h, k_spec * d, ss, k_spec * nps, x->hg,
-                     x->L[0].attn_norm, x->stream);
-        // the last draft layer hands its rows to the verify: FM row b*k_spec + j of hk_hg
-        dvi_status st = run_layers(x, 0, cf.split_k, B, 1, j, h, ss, x->hg, k_spec, x->hk_hg, k_spec, j);
-        if (st != DVI_OK) return st;
-        if (!x->ar_mode) {
-            void *xh = (uint8_t *)x->hk_hat + (size_t)j * d * x->es;
-            launch_head_prep(x->dt, h, k_spec * d, ss, k_spec * nps, x->final_norm, B, d, cf.rms_eps, x->lora_B,
-                             cf.lora_rank, xh, k_spec * d, x->dfm, x->lora_u, x->stream);
-            head(x, x->dfm, nullptr, 0, B, x->dlogits, true, x->drafts + j, k_spec, forced ? x->forced + j : nullptr);
+    const int nck = attn_chunks(x, max_len(x) + k_spec - 1);
+    const dvi_status st = run_pass(x, {0, B, k_spec, x->ar_mode + 2 * (forced != nullptr), nck}, [&]() -> dvi_status {
+        for (int j = 0; j < k_spec; ++j) {
+            // draft token j of sequence b lives in row b*k_spec + j of hk / hk_ss / hk_hg
+            const int32_t *tok = j == 0 ? x->pending : x->drafts + (j - 1);
+            float *h = x->hk + (size_t)j * d;
+            float *ss = x->hk_ss + (size_t)j * nps;
+            launch_embed(x->dt, x->emb, tok, j == 0 ? 1 : k_spec, B, 1, d, h, k_spec * d, ss, k_spec * nps, x->hg,
+                         x->L[0].attn_norm, x->stream);
+            // the last draft layer hands its rows to the verify: FM row b*k_spec + j of hk_hg
+            dvi_status sl = run_layers(x, 0, cf.split_k, B, 1, j, nck, h, ss, x->hg, k_spec, x->hk_hg, k_spec, j);
+            if (sl != DVI_OK) return sl;
+            if (!x->ar_mode) {
+                void *xh = (uint8_t *)x->hk_hat + (size_t)j * d * x->es;
+                launch_head_prep(x->dt, h, k_spec * d, ss, k_spec * nps, x->final_norm, B, d, cf.rms_eps, x->lora_B,
+                                 cf.lora_rank, xh, k_spec * d, x->dfm, x->lora_u, x->stream);
+                head(x, x->dfm, nullptr, 0, B, x->dlogits, true, x->drafts + j, k_spec,
+                     forced ? x->forced + j : nullptr);
+            }
         }
-    }
+        LAUNCHCHK(x);
+        return DVI_OK;
+    });
+    if (st != DVI_OK) return st;
     if (x->ar_mode) HIPCHK(x, hipMemsetAsync(x->drafts, 0xff, (size_t)B * 4, x->stream));
     ev_end(x, 0);
     LAUNCHCHK(x);
@@ -699,9 +765,16 @@ extern "C" dvi_status dvi_verify(dvi_ctx *x, int32_t *targets_out, int32_t *acce
     const dvi_config &cf = x->cfg;
     const int B = x->B, k = x->k_spec, M = B * k, d = cf.d_model;
     ev_begin(x, 1);
-    dvi_status st = run_layers(x, cf.split_k, cf.n_layers, B, k, 0, x->hk, x->hk_ss, x->hk_hg, 1, x->hk_hg, 1, 0);
+    const int nck = attn_chunks(x, max_len(x) + k - 1);
+    const dvi_status st = run_pass(x, {1, B, k, 0, nck}, [&]() -> dvi_status {
+        dvi_status sl =
+            run_layers(x, cf.split_k, cf.n_layers, B, k, 0, nck, x->hk, x->hk_ss, x->hk_hg, 1, x->hk_hg, 1, 0);
+        if (sl != DVI_OK) return sl;
+        head(x, x->hk_hg, x->hk_ss, d / 16, M, x->vlogits, false, x->targets, 1, nullptr);
+        LAUNCHCHK(x);
+        return DVI_OK;
+    });
     if (st != DVI_OK) return st;
-    head(x, x->hk_hg, x->hk_ss, d / 16, M, x->vlogits, false, x->targets, 1, nullptr);
     ev_end(x, 1);
     LAUNCHCHK(x);
     if (targets_out || accept_out) {
@@ -894,24 +967,28 @@ extern "C" dvi_status dvi_read_kv(dvi_ctx *x, int32_t layer, int32_t seq, int32_
         pos0 + npos > cf.max_seq)
         return fail(x, DVI_ERR_ARG, "read_kv range");
     const size_t es = x->es, hd = cf.head_dim, row = hd * es, cap = x->s_cap;
-    std::vector<uint8_t> vt((size_t)cf.n_kv_heads * hd * npos * es);
+    if (npos == 0) return DVI_OK;
+    // values are stored chunk-major ([pos / 64][hd][pos % 64]); fetch the whole chunks that
+    // cover the range, then gather
+    const int c0 = pos0 / 64, nc = (pos0 + npos - 1) / 64 - c0 + 1;
+    const size_t cbytes = hd * 64 * es;
+    std::vector<uint8_t> vt((size_t)cf.n_kv_heads * nc * cbytes);
     for (int h = 0; h < cf.n_kv_heads; ++h) {
         const size_t off = (((size_t)seq * cf.n_kv_heads + h) * cap + pos0) * row;
         HIPCHK(x, hipMemcpyAsync((uint8_t *)k + (size_t)h * npos * row, (uint8_t *)x->L[layer].Kc + off, npos * row,
                                  hipMemcpyDeviceToHost, x->stream));
-        // values are stored transposed ([head dim][position]); fetch the [hd, npos] block
-        const size_t voff = (((size_t)seq * cf.n_kv_heads + h) * hd * cap + pos0) * es;
-        if (npos > 0)
-            HIPCHK(x, hipMemcpy2DAsync(vt.data() + (size_t)h * hd * npos * es, npos * es,
-                                       (uint8_t *)x->L[layer].Vc + voff, cap * es, npos * es, hd,
-                                       hipMemcpyDeviceToHost, x->stream));
+        const size_t voff = ((size_t)seq * cf.n_kv_heads + h) * hd * cap * es + (size_t)c0 * cbytes;
+        HIPCHK(x, hipMemcpyAsync(vt.data() + (size_t)h * nc * cbytes, (uint8_t *)x->L[layer].Vc + voff, nc * cbytes,
+                                 hipMemcpyDeviceToHost, x->stream));
     }
     HIPCHK(x, hipStreamSynchronize(x->stream));
     for (int h = 0; h < cf.n_kv_heads; ++h)
-        for (int p = 0; p < npos; ++p)
+        for (int p = 0; p < npos; ++p) {
+            const int pa = pos0 + p, c = pa / 64 - c0, o = pa % 64;
             for (size_t d = 0; d < hd; ++d)
                 memcpy((uint8_t *)v + (((size_t)h * npos + p) * hd + d) * es,
-                       vt.data() + (((size_t)h * hd + d) * npos + p) * es, es);
+                       vt.data() + (((size_t)h * nc + c) * hd + d) * 64 * es + (size_t)o * es, es);
+        }
     return DVI_OK;
 }
 

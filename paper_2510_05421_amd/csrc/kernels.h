@@ -56,7 +56,7 @@ struct GemmArgs {
     // EPI_QKV
     float *Q;           // [M][n_heads * hd] fp32
     void *Kc, *Vc;      // this layer's caches: keys [max_batch][n_kv][s_max][hd], values
-                        // transposed [max_batch][n_kv][hd][s_max]
+                        // chunk-major [max_batch][n_kv][s_max / 64][hd][64]
     int n_heads, n_kv, hd, s_max;
     const float2 *rope; // [s_max][hd/2] (cos, sin)
     // EPI_SWIGLU
@@ -98,11 +98,13 @@ constexpr int kMaxBatch = 64;
 struct AttnArgs {
     const float *Q;      // [M][n_heads*hd]
     const void *Kc;      // [max_batch][n_kv][s_max][hd]
-    const void *Vc;      // [max_batch][n_kv][hd][s_max] (transposed)
-    int len[kMaxBatch];  // cache length of every sequence (passed by value: no dependent load)
+    const void *Vc;      // [max_batch][n_kv][s_max / 64][hd][64] (chunk-major)
+    const int32_t *lens; // [B] cache length of every sequence (device memory, so that a captured
+                         // graph replays with the current lengths)
     int B, c, pos_off;
     int n_heads, n_kv, hd, s_max;
-    int n_chunks;        // 64-key chunks of the longest context in this call
+    int n_chunks;        // grid: 64-key chunks of the longest context this launch may see (an upper
+                         // bound; workgroups past a sequence's own chunks exit at once)
     int chunk_stride;    // partial slots per (token, head) = ceil(s_max / 64)
     float scale;
     float *part_o;       // [M][n_heads][chunk_stride][hd]

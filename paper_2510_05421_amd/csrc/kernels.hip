@@ -84,6 +84,23 @@ __global__ void __launch_bounds__(64 * WMAX) gemm_kernel(GemmArgs a) {
 #pragma unroll
         for (int g = 0; g < MG; ++g) acc[t][g] = (f32x4){0.f, 0.f, 0.f, 0.f};
 
+    // Requested ahead of the weight stream (their latency then hides under it): the folded
+    // norm's partial sums of this wave's first token (K <= 5120), and the operands of the tile
+    // whose epilogue this wave will run.  Decode shapes only (up to 32 tokens); larger M keeps
+    // its registers for the accumulators and loads these after the stream.
+    constexpr bool kEarly = MG <= 2;
+    constexpr int SSP = 5;
+    const int nparts = a.K / 16;
+    const bool ss_early = kEarly && a.ss_in != nullptr && wave < a.M && nparts <= 64 * SSP;
+    float ssv[SSP];
+    if (ss_early) {
+        const float *src = a.ss_in + (size_t)wave * a.ld_ss_in;
+#pragma unroll
+        for (int k = 0; k < SSP; ++k) ssv[k] = src[min(lane + 64 * k, nparts - 1)];
+    }
+    EpiOperands<MG> pre;
+    if (kEarly && wave < RT) epilogue_prefetch<MG, EPI>(a, nt0 + wave, pre);
+
     // Each activation fragment feeds RT weight tiles.  The loop is software-pipelined: the
     // fragments of the next U chunks are requested before the current U are multiplied, so a
     // wave always has loads in flight while its MFMAs run.
@@ -101,6 +118,7 @@ __global__ void __launch_bounds__(64 * WMAX) gemm_kernel(GemmArgs a) {
         }
     };
     fetch(c0, w, x);
+    if (kEarly && wave < RT) epilogue_prefetch_rope<MG, EPI>(a, nt0 + wave, pre);
     for (int c = c0; c < c1; c += U) {
         uint4 wn[U][RT], xn[U][MG];
         fetch(c + U, wn, xn);
@@ -125,7 +143,8 @@ __global__ void __launch_bounds__(64 * WMAX) gemm_kernel(GemmArgs a) {
     __shared__ float sinv[64];
     if (a.ss_in != nullptr)
         for (int m = wave; m < a.M; m += nw) {
-            const float v = inv_rms(a.ss_in + (size_t)m * a.ld_ss_in, a.K / 16, a.K, a.eps);
+            const float v = (m == wave && ss_early) ? inv_rms_regs<SSP>(ssv, nparts, a.K, a.eps)
+                                                    : inv_rms(a.ss_in + (size_t)m * a.ld_ss_in, nparts, a.K, a.eps);
             if (lane == 0) sinv[m] = v;
         }
     f32x4 mine[MG];
@@ -144,7 +163,11 @@ __global__ void __launch_bounds__(64 * WMAX) gemm_kernel(GemmArgs a) {
     if (wave >= RT) return;
     const int nt = nt0 + wave;
 
-    gemm_epilogue<T, MG, EPI>(a, nt, mine, sinv);
+    if (!kEarly) {
+        epilogue_prefetch<MG, EPI>(a, nt, pre);
+        epilogue_prefetch_rope<MG, EPI>(a, nt, pre);
+    }
+    gemm_epilogue<T, MG, EPI>(a, nt, mine, sinv, pre);
 }
 
 // Launch shape of a weight matrix, a function of (N, K) only, never of M: RT 16-row tiles
@@ -345,8 +368,8 @@ void launch_lora_u(DType t, const void *x, const float *Bm, int M, int d, int r,
 //   S = Q K^T      A = query fragments, B = key fragments read straight from the key cache;
 //   softmax        per row over the chunk's 64 keys: max, p = exp(s - max), sum (fixed tree);
 //   O = P V        P goes through a per-wave LDS tile into A-operand layout; B = value
-//                  fragments read straight from the transposed value cache (positions
-//                  contiguous per head dim).
+//                  fragments read straight from the chunk-major value cache (one chunk's
+//                  [hd][64] block is contiguous, positions innermost).
 // Row at position p sees keys 0..p (block-causal); keys past a row's position, or past the
 // cached length, are masked before the max and multiply as zeros.  Each chunk's (max, sum,
 // unnormalised output) is published with agent-scope relaxed atomic stores; a per-(sequence,
@@ -355,6 +378,46 @@ void launch_lora_u(DType t, const void *x, const float *Bm, int M, int d, int r,
 // the loads stay in flight together.  Rows are independent MFMA rows and the chunk arithmetic
 // depends only on positions, so a row's result is the same whichever other rows share its block.
 // ------------------------------------------------------------------------------------------
+// One group of up to 64 chunks of a row's merge (lane = chunk for the statistics; lane holds
+// head dims PER*lane .. PER*lane + PER-1 of the outputs): the group's maximum and the rescaled sums come from wave reductions with
+// a fixed tree, and the partial outputs are folded in chunk order.  All NB chunks' loads are
+// unconditional (addresses clamped to the group's last chunk, weights of clamped lanes zero, so
+// they add zeros) and issued before the arithmetic that needs them: one round trip per group.
+// NB only sets how many loads are in flight; the sum is the same for every NB >= cn.
+template <int HD, int NB>
+__device__ __forceinline__ void merge_group(__amdgpu_buffer_rsrc_t mlr, __amdgpu_buffer_rsrc_t por, size_t slot,
+                                            int cn, int lane, float &Mr, float &L, float (&o)[HD / 64]) {
+    constexpr int PER = HD / 64;
+    const size_t sl = slot + min(lane, cn - 1);
+    const float my_m = ld_coherent_f32(mlr, (uint32_t)(sl * 8)), my_l = ld_coherent_f32(mlr, (uint32_t)(sl * 8 + 4));
+    float ov[NB][PER];
+#pragma unroll
+    for (int u = 0; u < NB; ++u) {
+        const uint32_t off = (uint32_t)(((slot + min(u, cn - 1)) * HD + PER * lane) * 4);
+        if (PER == 2) {
+            const float2 v = ld_coherent_f32x2(por, off);
+            ov[u][0] = v.x;
+            ov[u][PER - 1] = v.y;
+        } else {
+            ov[u][0] = ld_coherent_f32(por, off);
+        }
+    }
+    const float gm = wave_max(lane < cn ? my_m : -INFINITY);
+    const float Mn = fmaxf(Mr, gm);
+    const float rs = expf(Mr - Mn);  // 0 on the first group
+    const float scl = lane < cn ? expf(my_m - Mn) : 0.f;
+    L = L * rs + wave_sum(my_l * scl);
+#pragma unroll
+    for (int q = 0; q < PER; ++q) o[q] *= rs;
+    Mr = Mn;
+#pragma unroll
+    for (int u = 0; u < NB; ++u) {
+        const float sc = __shfl(scl, u);  // zero for chunks past cn
+#pragma unroll
+        for (int q = 0; q < PER; ++q) o[q] += ov[u][q] * sc;
+    }
+}
+
 constexpr long kAttnPackWaves = 2048;
 
 template <DType T, int HD, int WPB>
@@ -372,7 +435,7 @@ __global__ void __launch_bounds__(64 * WPB) attn_kernel(AttnArgs a) {
     const int kvh = blockIdx.y, b = blockIdx.z;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int l16 = lane & 15, lg = lane >> 4;
-    const int len0 = a.len[b] + a.pos_off;
+    const int len0 = a.lens[b] + a.pos_off;
     const int pmax = len0 + a.c - 1;
     const int nch = pmax / CK + 1;
     if (WPB * (int)blockIdx.x >= nch) return;  // uniform across the workgroup
@@ -383,50 +446,61 @@ __global__ void __launch_bounds__(64 * WPB) attn_kernel(AttnArgs a) {
     const int G = a.n_heads / a.n_kv;
     const int R = a.c * G;
     const size_t kc0 = ((size_t)b * a.n_kv + kvh) * a.s_max + kbase;          // key rows
-    const size_t vt0 = ((size_t)b * a.n_kv + kvh) * HD * a.s_max + kbase;      // value columns
+    const size_t vt0 = ((size_t)b * a.n_kv + kvh) * HD * a.s_max + (size_t)ch * HD * CK;  // value chunk
     const uint4 zero = {0u, 0u, 0u, 0u};
 
     if (active) {
+        // Query fragments of one 16-row tile: row r0 + l16, head dims step*KC + EPL*lg .. +EPL.
+        // Rows past R read row R-1 and are zeroed when packed.
+        float4 qraw[DS][EPL / 4];
+        auto load_q = [&](int r0) {
+            const int rr = min(r0 + l16, R - 1);
+            const int i = rr / G, gi = rr - i * G;
+            const float4 *qrow =
+                (const float4 *)(a.Q + ((size_t)(b * a.c + i) * a.n_heads + kvh * G + gi) * HD + EPL * lg);
+#pragma unroll
+            for (int st = 0; st < DS; ++st)
+#pragma unroll
+                for (int e4 = 0; e4 < EPL / 4; ++e4) qraw[st][e4] = qrow[(st * KC) / 4 + e4];
+        };
+        load_q(0);  // in flight together with the key and value fragments
         // Every position of a 64-key chunk lies inside the cache row (the row length is a multiple
-        // of 64), so the fragment loads are unconditional; keys at or past nk (not yet written,
-        // or past the block) are zeroed afterwards.
+        // of 64), so the fragment loads are unconditional.  Keys at or past nk (not yet written, or
+        // past the block) get score -inf below, whatever they hold, so key fragments need no mask.
         // key fragments: tile t holds keys 16t + l16; head dims step*KC + EPL*lg .. +EPL
         uint4 kf[4][DS];
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
-            const int key = 16 * t + l16;
-            const uint4 *src = (const uint4 *)((const E *)a.Kc + (kc0 + key) * HD + EPL * lg);
+            const uint4 *src = (const uint4 *)((const E *)a.Kc + (kc0 + 16 * t + l16) * HD + EPL * lg);
 #pragma unroll
-            for (int st = 0; st < DS; ++st) {
-                const uint4 v = src[st * (KC * sizeof(E) / 16)];
-                kf[t][st] = key < nk ? v : zero;
-            }
+            for (int st = 0; st < DS; ++st) kf[t][st] = src[st * (KC * sizeof(E) / 16)];
         }
-        // value fragments: tile dt holds head dim 16 dt + l16; keys step*KC + EPL*lg .. +EPL
+        // value fragments: tile dt holds head dim 16 dt + l16; keys step*KC + EPL*lg .. +EPL.  Their
+        // probabilities are zero, but 0 * (NaN or inf) is not, so those keys are zeroed.
         uint4 vf[DT][KS];
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
-            const E *src = (const E *)a.Vc + vt0 + (size_t)(16 * dt + l16) * a.s_max + EPL * lg;
+            const E *src = (const E *)a.Vc + vt0 + (16 * dt + l16) * CK + EPL * lg;
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks)
-                vf[dt][ks] = mask_keys<T>(*(const uint4 *)(src + ks * KC), ks * KC + EPL * lg, nk);
+            for (int ks = 0; ks < KS; ++ks) vf[dt][ks] = *(const uint4 *)(src + ks * KC);
         }
+        // keep every load above in flight before the first use of any of them
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) vf[dt][ks] = mask_keys<T>(vf[dt][ks], ks * KC + EPL * lg, nk);
         for (int r0 = 0; r0 < R; r0 += 16) {
-            // query fragments: row r0 + l16, head dims step*KC + EPL*lg .. +EPL
-            const int rq = r0 + l16;
+            if (r0 > 0) load_q(r0);
             uint4 qf[DS];
             {
-                const bool ok = rq < R;
-                const int rr = ok ? rq : R - 1;  // rows past R read row R-1 and are zeroed
-                const int i = rr / G, gi = rr - i * G;
-                const float4 *qrow =
-                    (const float4 *)(a.Q + ((size_t)(b * a.c + i) * a.n_heads + kvh * G + gi) * HD + EPL * lg);
+                const bool ok = r0 + l16 < R;
 #pragma unroll
                 for (int st = 0; st < DS; ++st) {
                     float v[EPL];
 #pragma unroll
                     for (int e4 = 0; e4 < EPL / 4; ++e4) {
-                        const float4 q4 = qrow[(st * KC) / 4 + e4];
+                        const float4 q4 = qraw[st][e4];
                         v[4 * e4 + 0] = ok ? q4.x : 0.f;
                         v[4 * e4 + 1] = ok ? q4.y : 0.f;
                         v[4 * e4 + 2] = ok ? q4.z : 0.f;
@@ -520,59 +594,30 @@ __global__ void __launch_bounds__(64 * WPB) attn_kernel(AttnArgs a) {
     }
     __syncthreads();
     if (!is_last) return;
-    // Merge, one wave per row.  Chunks are taken 64 at a time, lane = chunk: the group's
-    // maximum and the rescaled sums come from wave reductions with a fixed tree, and the partial
-    // outputs are folded in chunk order.  All loads are unconditional (addresses clamped to the
-    // row's last chunk, weights of clamped lanes zero) and issued before the arithmetic that
-    // needs them, so a row with up to 64 chunks costs one round trip.
-    constexpr int PER = HD / 64;
+    // Merge, one wave per row.
     const __amdgpu_buffer_rsrc_t mlr = coherent_rsrc(a.part_ml), por = coherent_rsrc(a.part_o);
     for (int row = w; row < R; row += WPB) {
         const int i = row / G, gi = row - i * G;
         const int m = b * a.c + i, h = kvh * G + gi;
         const int ncr = (len0 + i) / CK + 1;
         const size_t slot0 = ((size_t)m * a.n_heads + h) * a.chunk_stride;
-        float Mr = -INFINITY, L = 0.f, o[PER];
+        float Mr = -INFINITY, L = 0.f, o[HD / 64];
 #pragma unroll
-        for (int q = 0; q < PER; ++q) o[q] = 0.f;
+        for (int q = 0; q < HD / 64; ++q) o[q] = 0.f;
         for (int c0 = 0; c0 < ncr; c0 += 64) {
             const int cn = min(64, ncr - c0);
-            const size_t sl = slot0 + c0 + min(lane, cn - 1);
-            const float my_m = ld_coherent_f32(mlr, (uint32_t)(sl * 8)), my_l = ld_coherent_f32(mlr, (uint32_t)(sl * 8 + 4));
-            float ov[8][PER];
-#pragma unroll
-            for (int u = 0; u < 8; ++u)
-#pragma unroll
-                for (int q = 0; q < PER; ++q)
-                    ov[u][q] = ld_coherent_f32(por, (uint32_t)(((slot0 + c0 + min(u, cn - 1)) * HD + lane + 64 * q) * 4));
-            const float gm = wave_max(lane < cn ? my_m : -INFINITY);
-            const float Mn = fmaxf(Mr, gm);
-            const float rs = expf(Mr - Mn);  // 0 on the first group
-            const float scl = lane < cn ? expf(my_m - Mn) : 0.f;
-            L = L * rs + wave_sum(my_l * scl);
-#pragma unroll
-            for (int q = 0; q < PER; ++q) o[q] *= rs;
-            Mr = Mn;
-            for (int cb = 0; cb < cn; cb += 8) {
-                if (cb > 0) {
-#pragma unroll
-                    for (int u = 0; u < 8; ++u)
-#pragma unroll
-                        for (int q = 0; q < PER; ++q)
-                            ov[u][q] = ld_coherent_f32(
-                                por, (uint32_t)(((slot0 + c0 + min(cb + u, cn - 1)) * HD + lane + 64 * q) * 4));
-                }
-#pragma unroll
-                for (int u = 0; u < 8; ++u) {
-                    const float sc = __shfl(scl, cb + u);  // zero for chunks past cn
-#pragma unroll
-                    for (int q = 0; q < PER; ++q) o[q] += ov[u][q] * sc;
-                }
-            }
+            if (cn <= 8)
+                merge_group<HD, 8>(mlr, por, slot0 + c0, cn, lane, Mr, L, o);
+            else if (cn <= 16)
+                merge_group<HD, 16>(mlr, por, slot0 + c0, cn, lane, Mr, L, o);
+            else if (cn <= 32)
+                merge_group<HD, 32>(mlr, por, slot0 + c0, cn, lane, Mr, L, o);
+            else
+                merge_group<HD, 64>(mlr, por, slot0 + c0, cn, lane, Mr, L, o);
         }
 #pragma unroll
-        for (int q = 0; q < PER; ++q)
-            St<T>::store(a.O, fm_index<T>(m, h * HD + lane + 64 * q, a.n_heads * HD), o[q] / L);
+        for (int q = 0; q < HD / 64; ++q)
+            St<T>::store(a.O, fm_index<T>(m, h * HD + (HD / 64) * lane + q, a.n_heads * HD), o[q] / L);
     }
 }
 

@@ -91,7 +91,11 @@ class Engine:
         self.device = torch.device(device)
         self.lib = _abi.load()
         torch.cuda.set_device(self.device)
-        self.stream = torch.cuda.current_stream(self.device)
+        # The engine's own stream (default priority): the null stream cannot be captured into the
+        # HIP graphs that replay the draft and verify passes.  It starts after the work already
+        # queued on the current stream (the weight uploads below are ordered by the wait in front
+        # of dvi_create).
+        self.stream = torch.cuda.Stream(self.device)
         L = cfg.n_layers
         # frozen weights: only needed until dvi_create has copied them into the workspace
         frozen = {"tok_emb": _dev(weights.tok_emb, self.device), "final_norm": _dev(weights.final_norm, self.device),
@@ -111,6 +115,9 @@ class Engine:
             raise _abi.DVIError(_abi.ERR_ARG, "invalid configuration")
         self.workspace = torch.empty(nbytes + 256, dtype=torch.uint8, device=self.device)
         base = (self.workspace.data_ptr() + 255) & ~255
+        for t in (self.workspace, self.lora_A, self.lora_B):
+            t.record_stream(self.stream)
+        self.stream.wait_stream(torch.cuda.current_stream(self.device))
         ctx = ctypes.c_void_p()
         st = self.lib.dvi_create(ctypes.byref(self._ccfg), ctypes.byref(cw), base, nbytes,
                                  self.stream.cuda_stream, ctypes.byref(ctx))
@@ -130,8 +137,14 @@ class Engine:
 
     def close(self):
         if getattr(self, "ctx", None):
+            self.stream.synchronize()
             self.lib.dvi_destroy(self.ctx)
             self.ctx = None
+
+    def set_graphs(self, enable: bool):
+        """Replay the draft and verify passes as captured HIP graphs (the default) or launch
+        every kernel directly; results are bitwise the same."""
+        self._check(self.lib.dvi_set_graphs(self.ctx, 1 if enable else 0))
 
     def __del__(self):
         try:
@@ -197,6 +210,8 @@ class Engine:
                        beta1=0.9, beta2=0.999, eps=1e-8, opt_step=None, grads: bool = False):
         g_A = torch.empty_like(self.lora_A) if grads else None
         g_B = torch.empty_like(self.lora_B) if grads else None
+        if grads:
+            self.stream.wait_stream(torch.cuda.current_stream(self.device))
         if lr != 0.0 and opt_step is None:
             self.opt_step += 1
             opt_step = self.opt_step

@@ -285,3 +285,35 @@ def test_state_capacity_and_numeric_errors():
     assert e.value.status == ERR_NUMERIC
     eng.abort()
     eng.close()
+
+
+def test_graph_replay_equals_direct_launches():
+    """Draft and verify replayed from captured HIP graphs give the tokens, accept lengths, keys,
+    values and drafter updates of direct launches, bitwise.  The prompts end just before a
+    256-position attention-grid bucket edge, so generation re-captures there; drafter updates,
+    commits and plain-decoding steps run as direct launches between the replays."""
+    shape = gu.SHAPES["7b_L4"]
+    P, T, B = 236, 48, 2
+    prompts = synth.make_prompts(shape.vocab, B, P, 21)
+    w = synth.make_weights(shape, 0, lora_A_std=0.02)
+    runs = []
+    for graphs in (True, False):
+        eng, _ = gu.engine(shape, max_batch=B, max_seq=P + T + 16, weights=w)
+        eng.set_graphs(graphs)
+        toks, info = eng.generate(prompts, T, 4, update_every=3)
+        ar, _ = eng.generate(prompts, 12, 1)
+        lens = eng.lengths().copy()
+        kv = [eng.read_kv(l, b, 0, int(lens[b])) for l in range(shape.n_layers) for b in range(B)]
+        lora = (eng.lora_A.cpu().numpy(), eng.lora_B.cpu().numpy())
+        runs.append((toks, info, ar, kv, lora))
+        _say("graphs=%s: %d steps, mean m %.2f, %d updates" % (graphs, info["steps"], info["m"].mean(),
+                                                              len(info["updates"])))
+        eng.close()
+    (tg, ig, ag, kg, lg), (td, id_, ad, kd, ld) = runs
+    assert np.array_equal(tg, td) and np.array_equal(ag, ad)
+    assert np.array_equal(ig["m"], id_["m"]) and np.array_equal(ig["n"], id_["n"])
+    for (k1, v1), (k2, v2) in zip(kg, kd):
+        assert np.array_equal(k1, k2) and np.array_equal(v1, v2)
+    assert np.array_equal(lg[0], ld[0]) and np.array_equal(lg[1], ld[1])
+    for a, b in zip(ig["updates"], id_["updates"]):
+        assert a["loss"] == b["loss"] and a["rows"] == b["rows"]
