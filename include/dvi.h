@@ -72,7 +72,7 @@ typedef enum { DVI_FP32 = 0, DVI_BF16 = 1 } dvi_dtype;
 typedef struct {
     int32_t n_layers;      /* L                                                   */
     int32_t split_k;       /* k: draft = layers 1..k, verify = layers k+1..L      */
-    int32_t d_model;       /* multiple of 32                                      */
+    int32_t d_model;       /* multiple of 32, at most 8192                        */
     int32_t n_heads;
     int32_t n_kv_heads;
     int32_t head_dim;      /* 64 or 128                                           */

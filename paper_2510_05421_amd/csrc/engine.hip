@@ -239,6 +239,7 @@ static const char *check_config(const dvi_config *c) {
     if (c->n_layers < 1) return "n_layers < 1";
     if (c->split_k < 1 || c->split_k > c->n_layers) return "split_k must be in [1, n_layers]";
     if (c->d_model <= 0 || c->d_model % kc) return "d_model must be a positive multiple of 32 (bf16) / 16 (fp32)";
+    if (c->d_model > 8192) return "d_model must be <= 8192";
     if (c->head_dim != 64 && c->head_dim != 128) return "head_dim must be 64 or 128";
     if (c->n_heads < 1 || c->n_kv_heads < 1 || c->n_heads % c->n_kv_heads) return "n_heads must be a multiple of n_kv_heads";
     if ((c->n_heads * c->head_dim) % kc) return "n_heads*head_dim not a multiple of the K chunk";

@@ -251,26 +251,37 @@ void launch_gemm(DType t, Epi e, const GemmArgs &a, hipStream_t s, const LaunchE
 // Embedding gather (first layer input) and the draft-head preparation
 // ------------------------------------------------------------------------------------------
 // Row m = b*c + i takes token tok[b*tok_stride + i]: h = E[token] (fp32), its partial sums of
-// squares per 16 columns, and hg = dtype(h * g) for the first layer's folded RMSNorm.
+// squares per 16 columns, and hg = dtype(h * g) for the first layer's folded RMSNorm.  Thread t
+// holds columns 1024*kb + 4t .. +3 (d <= 8192); every load of the row is issued before the first
+// use (addresses clamped into the row, values of columns past d zeroed).
 template <DType T>
 __global__ void __launch_bounds__(256) embed_kernel(const void *emb, const int32_t *tok, int tok_stride, int c, int d,
                                                     float *h, int ldh, float *ss, int ld_ss, void *hg, const float *g) {
+    constexpr int KB = 8;
     const int m = blockIdx.x;
     const int b = m / c, i = m - b * c;
     const size_t row = (size_t)tok[(size_t)b * tok_stride + i] * d;
-    for (int base = 0; base < d; base += 1024) {
-        const int col = base + 4 * threadIdx.x;
-        const bool ok = col < d;
-        float v[4] = {0.f, 0.f, 0.f, 0.f};
-        if (ok)
+    float v[KB][4];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) v[j] = St<T>::load(emb, row + col + j);
-        const float s = sumsq16(v, 1);
+    for (int kb = 0; kb < KB; ++kb) {
+        const int col = min(kb * 1024 + 4 * (int)threadIdx.x, d - 4);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) v[kb][j] = St<T>::load(emb, row + col + j);
+    }
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+        if (kb * 1024 >= d) break;  // uniform
+        const int col = kb * 1024 + 4 * threadIdx.x;
+        const bool ok = col < d;
+        if (!ok)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) v[kb][j] = 0.f;
+        const float s = sumsq16(v[kb], 1);
         if (ok) {
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                h[(size_t)m * ldh + col + j] = v[j];
-                St<T>::store(hg, fm_index<T>(m, col + j, d), v[j] * g[col + j]);
+                h[(size_t)m * ldh + col + j] = v[kb][j];
+                St<T>::store(hg, fm_index<T>(m, col + j, d), v[kb][j] * g[col + j]);
             }
             if ((threadIdx.x & 3) == 0) ss[(size_t)m * ld_ss + col / 16] = s;
         }
@@ -288,21 +299,47 @@ void launch_embed(DType t, const void *emb, const int32_t *tok, int tok_stride, 
 // Draft head input: xhat = dtype(RMSNorm(h; g)) (the row the replay buffer logs and the head
 // GEMM reads) and the LoRA projection u[c] = sum_i B_s[c][i] xhat[i].  Workgroup (c, m).
 template <DType T>
-__global__ void __launch_bounds__(256) head_prep_kernel(const float *h, int ldh, const float *ss, int ld_ss,
-                                                        const float *g, int d, float eps, const float *Bm, int r,
-                                                        void *xhat, int ldx, void *xfm, float *u) {
+__global__ void __launch_bounds__(256) head_prep_kernel(const float *__restrict__ h, int ldh,
+                                                        const float *__restrict__ ss, int ld_ss,
+                                                        const float *__restrict__ g, int d, float eps,
+                                                        const float *__restrict__ Bm, int r, void *xhat, int ldx,
+                                                        void *xfm, float *u) {
+    // Thread t holds float4 columns t + 256k (d <= 8192); the row, gain and B_s row are
+    // requested together (addresses clamped, columns past d skipped), then used.
+    constexpr int KQ = 8;
     __shared__ float red[4];
     const int c = blockIdx.x, m = blockIdx.y;
+    const int n4 = d / 4;
+    const float4 *h4 = (const float4 *)(h + (size_t)m * ldh), *g4 = (const float4 *)g;
+    const float4 *b4 = (const float4 *)(Bm + (size_t)c * d);
+    float4 hv[KQ], gv[KQ], bv[KQ];
+#pragma unroll
+    for (int k = 0; k < KQ; ++k) {
+        const int q = min((int)threadIdx.x + 256 * k, n4 - 1);
+        hv[k] = h4[q];
+        gv[k] = g4[q];
+        bv[k] = b4[q];
+    }
     const float inv = inv_rms(ss + (size_t)m * ld_ss, d / 16, d, eps);
     float acc = 0.f;
-    for (int i = threadIdx.x; i < d; i += 256) {
-        float x = h[(size_t)m * ldh + i] * inv * g[i];
-        if (T == DType::BF16) x = bf2f(f2bf(x));
-        if (c == 0) {
-            St<T>::store(xhat, (size_t)m * ldx + i, x);
-            St<T>::store(xfm, fm_index<T>(m, i, d), x);
+#pragma unroll
+    for (int k = 0; k < KQ; ++k) {
+        const int q = threadIdx.x + 256 * k;
+        if (q < n4) {
+            const float hk[4] = {hv[k].x, hv[k].y, hv[k].z, hv[k].w};
+            const float gk[4] = {gv[k].x, gv[k].y, gv[k].z, gv[k].w};
+            const float bk[4] = {bv[k].x, bv[k].y, bv[k].z, bv[k].w};
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                float x = hk[j] * inv * gk[j];
+                if (T == DType::BF16) x = bf2f(f2bf(x));
+                if (c == 0) {
+                    St<T>::store(xhat, (size_t)m * ldx + 4 * q + j, x);
+                    St<T>::store(xfm, fm_index<T>(m, 4 * q + j, d), x);
+                }
+                acc += bk[j] * x;
+            }
         }
-        acc += Bm[(size_t)c * d + i] * x;
     }
     acc = block_sum256(acc, red);
     if (threadIdx.x == 0) u[(size_t)m * r + c] = acc;
@@ -654,6 +691,7 @@ __global__ void __launch_bounds__(256) argmax_kernel(const float *pv, const int3
     const int m = blockIdx.x;
     float best = -INFINITY;
     int bidx = 0x3fffffff, bad = 0;
+#pragma unroll 8
     for (int t = threadIdx.x; t < ntiles; t += 256) {
         const float v = pv[(size_t)m * ntiles + t];
         const int code = pi[(size_t)m * ntiles + t];
@@ -754,21 +792,30 @@ __global__ void commit_kernel(CommitArgs a) {
 
 void launch_commit(const CommitArgs &a, hipStream_t s) { commit_kernel<<<1, 64, 0, s>>>(a); }
 
-__global__ void ring_copy_kernel(const int32_t *cl, const uint8_t *hk, int row_bytes, const float *vl, int V,
-                                 uint8_t *rh, float *rl) {
+// Copy of the listed rows into their ring slots: row e of the list goes src -> slot, its state
+// row (row_bytes) and logits row (V floats), each split over gridDim.y blocks in 16-byte steps.
+__device__ __forceinline__ void copy16(uint8_t *__restrict__ dst, const uint8_t *__restrict__ src, size_t bytes) {
+    const size_t step = (size_t)gridDim.y * blockDim.x * 16;
+#pragma unroll 4
+    for (size_t k = ((size_t)blockIdx.y * blockDim.x + threadIdx.x) * 16; k < bytes; k += step)
+        *(uint4 *)(dst + k) = *(const uint4 *)(src + k);
+}
+
+__global__ void __launch_bounds__(256) ring_copy_kernel(const int32_t *cl, const uint8_t *hk, int row_bytes,
+                                                        const float *vl, int V, uint8_t *rh, float *rl) {
     const int e = blockIdx.x;
     if (e >= cl[0]) return;
     const int src = cl[1 + 2 * e], slot = cl[2 + 2 * e];
-    for (int k = threadIdx.x * 4; k < row_bytes; k += blockDim.x * 4)
-        *(uint32_t *)(rh + (size_t)slot * row_bytes + k) = *(const uint32_t *)(hk + (size_t)src * row_bytes + k);
-    for (int k = threadIdx.x; k < V; k += blockDim.x) rl[(size_t)slot * V + k] = vl[(size_t)src * V + k];
+    copy16(rh + (size_t)slot * row_bytes, hk + (size_t)src * row_bytes, (size_t)row_bytes);
+    copy16((uint8_t *)(rl + (size_t)slot * V), (const uint8_t *)(vl + (size_t)src * V), (size_t)V * 4);
 }
 
 void launch_ring_copy(const int32_t *cl, int max_rows, const void *hk_hat, int d, int es, const float *vlogits, int V,
                       void *ring_h, float *ring_logits, hipStream_t s) {
+    // row_bytes = d * es and V * 4 are multiples of 16 (d and V are multiples of 16)
     if (max_rows > 0)
-        ring_copy_kernel<<<max_rows, 256, 0, s>>>(cl, (const uint8_t *)hk_hat, d * es, vlogits, V, (uint8_t *)ring_h,
-                                                  ring_logits);
+        ring_copy_kernel<<<dim3(max_rows, 8), 256, 0, s>>>(cl, (const uint8_t *)hk_hat, d * es, vlogits, V,
+                                                           (uint8_t *)ring_h, ring_logits);
 }
 
 // ------------------------------------------------------------------------------------------
