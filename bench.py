@@ -85,6 +85,8 @@ def main():
     ap.add_argument("--steps", type=int, default=None)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="7b")
+    ap.add_argument("--no-ceiling", action="store_true",
+                    help="skip the full-acceptance leg (drafts forced to the greedy continuation)")
     ap.add_argument("--k-spec", type=int, default=None)
     ap.add_argument("--probe", default="gate_up", choices=sorted(KERNEL_NAMES))
     ap.add_argument("--probe-steps", type=int, default=20)
@@ -141,9 +143,9 @@ def main():
     remaining = np.full(B, N - 1, np.int32)
     state = {"step": 0}
 
-    def step(kk, stats=None, update=True):
+    def step(kk, stats=None, update=True, forced=None):
         lens_before = eng_lens[:]
-        eng.draft(kk)
+        eng.draft(kk, forced=forced)
         eng.verify()
         tok, n, m = eng.commit(max_new=remaining)
         remaining[:] = remaining - n
@@ -256,6 +258,36 @@ def main():
         ar_tps = sa["tokens"] / (a1 - a0)
         ar = {"tokens_per_s": round(ar_tps, 2), "steps": KA, "speedup": round(value / ar_tps, 3)}
         log("plain AR on the same engine: %.1f tokens/s -> speedup %.2fx" % (ar_tps, value / ar_tps))
+    # Full-acceptance ceiling: the same step with every draft forced to the verifier's own greedy
+    # continuation (taken from a plain-decoding run), so each step commits k_spec tokens.  The
+    # drafter head still runs in full (its argmax is replaced afterwards); no drafter updates.
+    ceil = None
+    if not args.no_ceiling:
+        NG = (W + K) * k + 1
+        greedy, _ = eng.generate(prompts, NG, 1)
+        eng.prefill(prompts)
+        remaining[:] = N - 1
+        eng_lens[:] = [P] * B
+        for s_ in range(W):
+            step(k, update=False, forced=greedy[:, s_ * k + 1:s_ * k + k + 1])
+        sc = {"tokens": 0, "m": [], "n": [], "verify_ms": [], "draft_ms": [], "verify_bytes": [], "draft_bytes": [],
+              "update_ms": [], "update_rows": []}
+        torch.cuda.synchronize()
+        c0 = time.perf_counter()
+        for s_ in range(W, W + K):
+            step(k, sc, update=False, forced=greedy[:, s_ * k + 1:s_ * k + k + 1])
+        torch.cuda.synchronize()
+        c1 = time.perf_counter()
+        mc = np.array(sc["m"])
+        ceil_tps = sc["tokens"] / (c1 - c0)
+        ceil = {"tokens_per_s": round(ceil_tps, 2), "steps": K, "ms_per_step": round(1e3 * (c1 - c0) / K, 4),
+                "mean_m": round(float(mc.mean()), 4), "tokens_per_step": round(sc["tokens"] / (K * B), 4),
+                "verify_ms": round(float(np.median(sc["verify_ms"])), 4),
+                "draft_ms": round(float(np.median(sc["draft_ms"])), 4),
+                "speedup_vs_ar": round(ceil_tps / ar["tokens_per_s"], 3) if ar else None}
+        log("full-acceptance ceiling (drafts forced to the greedy continuation): %.1f tokens/s, mean m %.2f, "
+            "%.2f ms/step%s" % (ceil_tps, mc.mean(), ceil["ms_per_step"],
+                                 " -> %.2fx plain AR" % ceil["speedup_vs_ar"] if ar else ""))
     eng.close()
     del eng
 
@@ -300,6 +332,7 @@ def main():
         "acceptance": {"mean_m": round(float(mv.mean()), 4), "mean_tokens_per_step": round(float(nv.mean()), 4),
                        "rate": round(float(mv.mean()) / k, 4)},
         "ar_baseline": ar,
+        "full_acceptance": ceil,
         "drafter_update": upd,
         "paper_context": PAPER_CONTEXT,
     }

@@ -166,6 +166,8 @@ WORKLOADS: Dict[str, Workload] = {
     "7b": Workload("7b", SHAPE_7B, 1, 512, 512, (4, 6, 8)),
     "7b_b8": Workload("7b_b8", SHAPE_7B, 8, 2048, 256, (8,)),
     "13b": Workload("13b", SHAPE_13B, 1, 1024, 512, (6,), update_every=8, buffer_rows=256),
+    # the 7B shape at the split the paper itself runs (drafter = layers 1..2 of 32), same weights
+    "7b_k2": Workload("7b_k2", SHAPE_7B.replace(name="7b_k2", split_k=2), 1, 512, 512, (4,)),
 }
 
 

@@ -31,10 +31,11 @@ def weights_cache():
 
 
 def _weights(cache, shape):
-    if shape.name not in cache:
+    key = shape.replace(name="", split_k=1)  # the weights depend on the dimensions only
+    if key not in cache:
         cache.clear()
-        cache[shape.name] = synth.make_weights(shape, 0)
-    return cache[shape.name]
+        cache[key] = synth.make_weights(shape, 0)
+    return cache[key]
 
 
 @pytest.mark.parametrize("name", list(FULL))
@@ -89,10 +90,11 @@ def _check_lossless(eng, shape, prompts, n_new, k_specs, update_every=0):
     return ar
 
 
-@pytest.mark.parametrize("wl", ["1b", "7b", "13b"])
+@pytest.mark.parametrize("wl", ["1b", "7b", "7b_k2", "13b"])
 def test_fullsize_speculative_equals_greedy(wl, weights_cache):
     """Every full workload (prompt length, new tokens, k_spec) commits greedy decoding's tokens
-    and keys/values bitwise; the 13B workload runs its drafter update every 8 steps."""
+    and keys/values bitwise; the 13B workload runs its drafter update every 8 steps.  7b_k2 is
+    the 7B model (same weights) split after layer 2: its greedy output is the 7B golden's."""
     W = synth.WORKLOADS[wl]
     shape = W.model
     k_specs = W.k_spec
@@ -102,8 +104,9 @@ def test_fullsize_speculative_equals_greedy(wl, weights_cache):
     eng, _ = gu.engine(shape, max_batch=W.batch, max_seq=W.prompt_len + W.new_tokens + 8,
                        weights=_weights(weights_cache, shape))
     ar = _check_lossless(eng, shape, prompts, W.new_tokens, k_specs, update_every=W.update_every)
-    if wl in FULL:
-        g = gu.golden(wl)
+    gname = {"7b_k2": "7b"}.get(wl, wl)
+    if gname in FULL:
+        g = gu.golden(gname)
         assert np.array_equal(g["prompt"], prompts[0])
         gu.compare_free_running(ar[0], g["tokens"], g["gaps"])
     eng.close()

@@ -205,6 +205,43 @@ def test_drafter_update_gradients_match_oracle(name, n_rows):
     eng.close()
 
 
+# The paper's objective ablations and drafter variants as coefficient vectors of the one loss.
+OBJECTIVES = {
+    "kl_only": oupd.Coeffs(c_kl=1.0, c_ce=0.0, c_pg=0.0, c_ent=0.0, tau=1.0, baseline=0.0),
+    "ce_only": oupd.Coeffs(c_kl=0.0, c_ce=1.0, c_pg=0.0, c_ent=0.0, tau=1.0, baseline=0.0),
+    "pg_only": oupd.Coeffs(c_kl=0.0, c_ce=0.0, c_pg=1.0, c_ent=0.0, tau=1.0, baseline=0.4),
+    "entropy_only": oupd.Coeffs(c_kl=0.0, c_ce=0.0, c_pg=0.0, c_ent=0.5, tau=1.0, baseline=0.0),
+    "tau_0.5": oupd.Coeffs(c_kl=1.0, c_ce=0.5, c_pg=0.5, c_ent=0.0, tau=0.5, baseline=0.2),
+    "tau_2": oupd.Coeffs(c_kl=1.0, c_ce=0.0, c_pg=0.0, c_ent=0.1, tau=2.0, baseline=0.0),
+}
+
+
+@pytest.mark.parametrize("obj", list(OBJECTIVES))
+def test_drafter_update_objective_variants(obj):
+    """Each objective alone (KL, reward-masked CE, policy gradient, entropy bonus) and
+    temperatures other than 1: gradients and loss terms against the oracle."""
+    shape = gu.SHAPES["1b_L4"]
+    n_rows = 128
+    c = OBJECTIVES[obj]
+    eng, w = gu.engine(shape, max_seq=64, lora_A_std=0.02, buffer_rows=256)
+    buf = synth.make_buffer(shape.d_model, shape.vocab, n_rows, seed=13)
+    assert 0 < buf.r.sum() < n_rows
+    eng.prefill(synth.make_prompts(shape.vocab, 1, 8, 1))
+    eng.write_buffer(buf.h, buf.a, buf.logits, buf.r, buf.fresh)
+    st = eng.update_drafter(c.c_kl, c.c_ce, c.c_pg, c.c_ent, c.tau, c.baseline, lr=0.0, grads=True)
+    W = w.as_f32(w.lm_head).astype(np.float64)
+    ref = oupd.loss_and_grad(W, w.lora_A.astype(np.float64), w.lora_B.astype(np.float64), shape.lora_gamma,
+                             buf.h.astype(np.float64), buf.a, buf.logits, buf.r, buf.fresh, c)
+    eA = gu.rel_l2(st["grad_A"].cpu().numpy(), ref.dA)
+    eB = gu.rel_l2(st["grad_B"].cpu().numpy(), ref.dB)
+    _say("objective %s: |dA| rel err %.3g, |dB| rel err %.3g, loss %.6g vs %.6g" % (obj, eA, eB, st["loss"], ref.loss))
+    assert eA <= 1e-2 and eB <= 1e-2
+    assert abs(st["loss"] - ref.loss) <= 1e-3 * max(1.0, abs(ref.loss))
+    for key in ("kl", "ce", "pg", "entropy"):
+        assert abs(st[key] - getattr(ref, key)) <= 1e-3 * max(1.0, abs(getattr(ref, key))), key
+    eng.close()
+
+
 def test_batched_sequences_are_independent():
     """Batch of 4 equals four single-sequence runs, token for token and bitwise in KV."""
     shape = gu.SHAPES["7b_L4"]
