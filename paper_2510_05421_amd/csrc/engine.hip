@@ -76,7 +76,7 @@ struct dvi_ctx {
     int32_t *ring_a, *ring_i, *ring_prev;
     int8_t *ring_r, *ring_fresh;
     // update
-    float *upd_Z, *upd_stats, *upd_dA, *upd_du, *upd_dB, *upd_loss, *upd_u;
+    float *upd_Z, *upd_stats, *upd_dA, *upd_du, *upd_dup, *upd_dB, *upd_loss, *upd_u;
     float *mA, *vA, *mB, *vB;
     // host mirror
     int state = S_CREATED;
@@ -205,6 +205,7 @@ static size_t layout(dvi_ctx *x, const dvi_config &c, void *base) {
     float *upd_stats = b.take<float>(R * 8 * 4);
     float *upd_dA = b.take<float>(V * r * 4);
     float *upd_du = b.take<float>(R * r * 4);
+    float *upd_dup = b.take<float>(R * kDuSlices * r * 4);
     float *upd_dB = b.take<float>(r * d * 4);
     float *upd_loss = b.take<float>(16 * 4);
     float *mA = b.take<float>(V * r * 4);
@@ -225,7 +226,7 @@ static size_t layout(dvi_ctx *x, const dvi_config &c, void *base) {
         x->prow = prow;
         x->ring_h = ring_h; x->ring_logits = ring_logits; x->ring_a = ring_a; x->ring_i = ring_i;
         x->ring_prev = ring_prev; x->ring_r = ring_r; x->ring_fresh = ring_fresh;
-        x->upd_Z = upd_Z; x->upd_stats = upd_stats; x->upd_dA = upd_dA; x->upd_du = upd_du; x->upd_dB = upd_dB;
+        x->upd_Z = upd_Z; x->upd_stats = upd_stats; x->upd_dA = upd_dA; x->upd_du = upd_du; x->upd_dup = upd_dup; x->upd_dB = upd_dB;
         x->upd_loss = upd_loss; x->upd_u = lora_u;
         x->mA = mA; x->vA = vA; x->mB = mB; x->vB = vB;
     }
@@ -922,6 +923,7 @@ extern "C" dvi_status dvi_update_drafter(dvi_ctx *x, const dvi_update_args *ua, 
     u.row_stats = x->upd_stats;
     u.dA = x->upd_dA;
     u.du = x->upd_du;
+    u.du_part = x->upd_dup;
     u.dB = x->upd_dB;
     u.loss_out = x->upd_loss;
     u.xfm = x->ufm;

@@ -145,6 +145,8 @@ void launch_ring_copy(const int32_t *copy_list, int max_rows, const void *hk_hat
                       const float *vlogits, int V, void *ring_h, float *ring_logits, hipStream_t s);
 
 // ---- drafter update (Section 3.4) ----
+constexpr int kDuSlices = 8;  // vocabulary slices of the du reduction
+
 struct UpdateArgs {
     const void *W;          // packed lm_head [V][d]
     const void *Hh;         // ring h_hat [rows][d] (dtype)
@@ -162,6 +164,7 @@ struct UpdateArgs {
     float *row_stats;       // [n][8]
     float *dA;              // [V][r]
     float *du;              // [n][r]
+    float *du_part;         // [n][kDuSlices][r] scratch: du over slices of the vocabulary
     float *dB;              // [r][d]
     float *loss_out;        // [16]: loss, kl, ce, pg, entropy, n, n_acc, n_fresh, n_fresh_acc | counts at [12..16)
 };

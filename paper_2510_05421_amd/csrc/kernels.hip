@@ -691,7 +691,6 @@ __global__ void __launch_bounds__(256) argmax_kernel(const float *pv, const int3
     const int m = blockIdx.x;
     float best = -INFINITY;
     int bidx = 0x3fffffff, bad = 0;
-#pragma unroll 8
     for (int t = threadIdx.x; t < ntiles; t += 256) {
         const float v = pv[(size_t)m * ntiles + t];
         const int code = pi[(size_t)m * ntiles + t];
@@ -948,67 +947,80 @@ __global__ void upd_loss_kernel(UpdateArgs u, const float *counts) {
 // unrolled and guarded by the rank so the slots stay in registers.
 constexpr int kMaxRank = 64;
 
-// dA[v][c] = gamma * sum_i g[i][v] u[i][c]   (one thread per vocabulary row v; rows i in order).
-// The workgroup stages u for up to 256 rows in LDS and walks the rows in blocks of that size.
+// dA[v][c] = gamma * sum_i g[i][v] u[i][c].  A workgroup takes 64 vocabulary rows (lane = row);
+// wave w takes the ranks c = w, w+4, ...  Rows i are taken 16 at a time with all 16 loads of g
+// in flight; each output is one sum over i in order.
 __global__ void __launch_bounds__(256) upd_dA_kernel(UpdateArgs u) {
-    __shared__ float us[256 * kMaxRank];
-    const int v = blockIdx.x * 256 + threadIdx.x;
-    float acc[kMaxRank];
+    constexpr int CPW = kMaxRank / 4;
+    const int lane = threadIdx.x & 63;
+    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int v = blockIdx.x * 64 + lane;
+    const int vv = min(v, u.V - 1);
+    float acc[CPW];
 #pragma unroll
-    for (int c = 0; c < kMaxRank; ++c) acc[c] = 0.f;
-    for (int i0 = 0; i0 < u.n; i0 += 256) {
-        const int ni = min(256, u.n - i0);
-        __syncthreads();
-        for (int e = threadIdx.x; e < ni * u.rank; e += 256) us[e] = u.u[(size_t)i0 * u.rank + e];
-        __syncthreads();
-        if (v < u.V) {
-#pragma unroll 4
-            for (int i = 0; i < ni; ++i) {
-                const float g = u.Z[(size_t)(i0 + i) * u.V + v];
+    for (int k = 0; k < CPW; ++k) acc[k] = 0.f;
+    for (int i0 = 0; i0 < u.n; i0 += 16) {
+        float g[16];
 #pragma unroll
-                for (int c = 0; c < kMaxRank; ++c)
-                    if (c < u.rank) acc[c] += g * us[i * u.rank + c];
-            }
+        for (int j = 0; j < 16; ++j) g[j] = u.Z[(size_t)min(i0 + j, u.n - 1) * u.V + vv];
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            if (i0 + j >= u.n) break;  // uniform
+            const float *ui = u.u + (size_t)(i0 + j) * u.rank;
+#pragma unroll
+            for (int k = 0; k < CPW; ++k)
+                if (w + 4 * k < u.rank) acc[k] += g[j] * ui[w + 4 * k];
         }
     }
     if (v < u.V)
 #pragma unroll
-        for (int c = 0; c < kMaxRank; ++c)
-            if (c < u.rank) u.dA[(size_t)v * u.rank + c] = u.gamma * acc[c];
+        for (int k = 0; k < CPW; ++k)
+            if (w + 4 * k < u.rank) u.dA[(size_t)v * u.rank + w + 4 * k] = u.gamma * acc[k];
 }
 
-// du[i][c] = gamma * sum_v A[v][c] g[i][v]   (one 512-thread workgroup per row i).  Thread t
-// takes v = t, t+512, ... in order, reading whole rows of A (16-byte loads), and the 512 partial
-// vectors are summed in a fixed tree (butterfly per wave, then the waves in order).
-__global__ void __launch_bounds__(512) upd_du_kernel(UpdateArgs u) {
-    __shared__ float part[8][kMaxRank + 1];
-    const int i = blockIdx.x, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+// du[i][c] = gamma * sum_v A[v][c] g[i][v], in two passes.  Pass 1: workgroup (i, s) sums the
+// vocabulary slice s (kDuSlices slices); thread t takes v = t, t+256, ... of the slice, four at a
+// time with their loads in flight, and the 256 partial vectors are summed in a fixed tree
+// (butterfly per wave, then the waves in order).  Pass 2 adds the slices in order.
+__global__ void __launch_bounds__(256) upd_du_kernel(UpdateArgs u) {
+    __shared__ float part[4][kMaxRank + 1];
+    const int i = blockIdx.x, s = blockIdx.y, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int span = (u.V + kDuSlices - 1) / kDuSlices;
+    const int v0 = s * span, v1 = min(u.V, v0 + span);
     float acc[kMaxRank];
 #pragma unroll
     for (int c = 0; c < kMaxRank; ++c) acc[c] = 0.f;
     const float *g = u.Z + (size_t)i * u.V;
     const bool vec = (u.rank & 3) == 0;
-#pragma unroll 4
-    for (int v = threadIdx.x; v < u.V; v += 512) {
-        const float gv = g[v];
-        const float *Av = u.A + (size_t)v * u.rank;
-        if (vec) {
+    for (int vb = v0 + threadIdx.x; vb < v1; vb += 4 * 256) {
+        // rows past the slice read its last row and enter with weight 0
+        float gv[4];
 #pragma unroll
-            for (int c4 = 0; c4 < kMaxRank / 4; ++c4)
-                if (4 * c4 < u.rank) {
-                    const float4 a4 = ((const float4 *)Av)[c4];
-                    acc[4 * c4 + 0] += a4.x * gv;
-                    acc[4 * c4 + 1] += a4.y * gv;
-                    acc[4 * c4 + 2] += a4.z * gv;
-                    acc[4 * c4 + 3] += a4.w * gv;
-                }
-        } else {
+        for (int q = 0; q < 4; ++q) {
+            const int v = vb + 256 * q;
+            const float gl = g[min(v, v1 - 1)];
+            gv[q] = v < v1 ? gl : 0.f;
+        }
 #pragma unroll
-            for (int c = 0; c < kMaxRank; ++c)
-                if (c < u.rank) acc[c] += Av[c] * gv;
+        for (int q = 0; q < 4; ++q) {
+            const float *Av = u.A + (size_t)min(vb + 256 * q, v1 - 1) * u.rank;
+            if (vec) {
+#pragma unroll
+                for (int c4 = 0; c4 < kMaxRank / 4; ++c4)
+                    if (4 * c4 < u.rank) {
+                        const float4 a4 = ((const float4 *)Av)[c4];
+                        acc[4 * c4 + 0] += a4.x * gv[q];
+                        acc[4 * c4 + 1] += a4.y * gv[q];
+                        acc[4 * c4 + 2] += a4.z * gv[q];
+                        acc[4 * c4 + 3] += a4.w * gv[q];
+                    }
+            } else {
+#pragma unroll
+                for (int c = 0; c < kMaxRank; ++c)
+                    if (c < u.rank) acc[c] += Av[c] * gv[q];
+            }
         }
     }
-    // fixed tree: butterfly inside each wave, then the 8 wave sums in order
 #pragma unroll
     for (int c = 0; c < kMaxRank; ++c)
         if (c < u.rank) {
@@ -1017,10 +1029,19 @@ __global__ void __launch_bounds__(512) upd_du_kernel(UpdateArgs u) {
         }
     __syncthreads();
     if (threadIdx.x < u.rank) {
-        float s = 0.f;
-        for (int t = 0; t < 8; ++t) s += part[t][threadIdx.x];
-        u.du[(size_t)i * u.rank + threadIdx.x] = u.gamma * s;
+        float t = 0.f;
+        for (int k = 0; k < 4; ++k) t += part[k][threadIdx.x];
+        u.du_part[((size_t)i * kDuSlices + s) * u.rank + threadIdx.x] = t;
     }
+}
+
+__global__ void upd_du_sum_kernel(UpdateArgs u) {
+    const int e = blockIdx.x * blockDim.x + threadIdx.x;
+    if (e >= u.n * u.rank) return;
+    const int i = e / u.rank, c = e - i * u.rank;
+    float t = 0.f;
+    for (int s = 0; s < kDuSlices; ++s) t += u.du_part[((size_t)i * kDuSlices + s) * u.rank + c];
+    u.du[e] = u.gamma * t;
 }
 
 // dB[c][k] = sum_i du[i][c] h[i][k]   (one thread per (k, c); rows i in order)
@@ -1035,12 +1056,13 @@ __global__ void __launch_bounds__(256) upd_dB_kernel(UpdateArgs u) {
 }
 
 // Drafter logits of the replay rows on MFMA: Z[m][v] = X[m] . W[v] + gamma * sum_c A[v][c] u[m][c]
-// for up to 256 rows m (X fragment-major, up to 16 groups of 16).  A workgroup owns a band of 8
+// for 65 to 256 rows m (X fragment-major, up to 16 groups of 16; up to 64 rows take the decode
+// GEMM, whose K split keeps each wave's chain of loads short).  A workgroup owns a band of 8
 // weight tiles (128 vocabulary rows); wave w takes tiles 2w and 2w+1 for every row group, so the
 // weights leave HBM once and each activation fragment, read by all four waves of the compute
 // unit, mostly hits L1.  Steps are software-pipelined two deep; fragments past the band or the
 // rows load a valid address and enter as zeros, so every MFMA runs unconditionally (MFMA does
-// not honour the EXEC mask).  kUpdG row groups per launch (4, 8 or 16, the rows rounded up),
+// not honour the EXEC mask).  kUpdG row groups per launch (8 or 16, the rows rounded up),
 // kUpdU steps in flight (deeper when the groups are fewer).
 constexpr int kUpdBand = 8, kUpdTW = 2;
 template <DType T, int kUpdG, int kUpdU>
@@ -1117,17 +1139,30 @@ void launch_update_forward(DType t, const UpdateArgs &u, hipStream_t s) {
         launch_gather_fm(t, u.Hh, false, 1, r0, rows, u.d, u.xfm, s);
         const float *ur = u.u + (size_t)r0 * u.rank;
         float *Zr = u.Z + (size_t)r0 * u.V;
-        if (t == DType::BF16) {
-            if (rows <= 64)
-                upd_gemm_kernel<DType::BF16, 4, 4><<<bands, 256, 0, s>>>(u.W, u.xfm, rows, u.V, u.d, u.A, ur, u.rank, u.gamma, Zr);
-            else if (rows <= 128)
+        if (rows <= 64) {
+            // up to four row groups: the decode GEMM (K split over the waves) with its LoRA
+            // epilogue streams the head fastest
+            GemmArgs g{};
+            g.W = u.W;
+            g.X = u.xfm;
+            g.M = rows;
+            g.N = u.V;
+            g.K = u.d;
+            g.Z = Zr;
+            g.part_val = u.part_val;
+            g.part_idx = u.part_idx;
+            g.lora_A = u.A;
+            g.lora_u = ur;
+            g.r = u.rank;
+            g.gamma = u.gamma;
+            launch_gemm(t, EPI_LOGITS, g, s);
+        } else if (t == DType::BF16) {
+            if (rows <= 128)
                 upd_gemm_kernel<DType::BF16, 8, 3><<<bands, 256, 0, s>>>(u.W, u.xfm, rows, u.V, u.d, u.A, ur, u.rank, u.gamma, Zr);
             else
                 upd_gemm_kernel<DType::BF16, 16, 2><<<bands, 256, 0, s>>>(u.W, u.xfm, rows, u.V, u.d, u.A, ur, u.rank, u.gamma, Zr);
         } else {
-            if (rows <= 64)
-                upd_gemm_kernel<DType::F32, 4, 4><<<bands, 256, 0, s>>>(u.W, u.xfm, rows, u.V, u.d, u.A, ur, u.rank, u.gamma, Zr);
-            else if (rows <= 128)
+            if (rows <= 128)
                 upd_gemm_kernel<DType::F32, 8, 3><<<bands, 256, 0, s>>>(u.W, u.xfm, rows, u.V, u.d, u.A, ur, u.rank, u.gamma, Zr);
             else
                 upd_gemm_kernel<DType::F32, 16, 2><<<bands, 256, 0, s>>>(u.W, u.xfm, rows, u.V, u.d, u.A, ur, u.rank, u.gamma, Zr);
@@ -1138,8 +1173,9 @@ void launch_update_forward(DType t, const UpdateArgs &u, hipStream_t s) {
 }
 
 void launch_update_backward(DType t, const UpdateArgs &u, hipStream_t s) {
-    upd_dA_kernel<<<(u.V + 255) / 256, 256, 0, s>>>(u);
-    upd_du_kernel<<<u.n, 512, 0, s>>>(u);
+    upd_dA_kernel<<<(u.V + 63) / 64, 256, 0, s>>>(u);
+    upd_du_kernel<<<dim3(u.n, kDuSlices), 256, 0, s>>>(u);
+    upd_du_sum_kernel<<<(u.n * u.rank + 255) / 256, 256, 0, s>>>(u);
     if (t == DType::BF16)
         upd_dB_kernel<DType::BF16><<<dim3((u.d + 255) / 256, u.rank), 256, 0, s>>>(u);
     else
