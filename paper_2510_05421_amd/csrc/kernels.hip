@@ -197,7 +197,7 @@ static GemmShape gemm_shape(int N, int K, int KC, int M) {
 template <typename Arg>
 static void launch_timed(void (*kernel)(Arg), dim3 grid, dim3 block, hipStream_t s, const LaunchEvents &ev,
                          const Arg &a) {
-    if (ev.start)
+    if (ev.start || ev.stop)  // either may be null: one interval can span several launches
         hipExtLaunchKernelGGL(kernel, grid, block, 0, s, ev.start, ev.stop, 0, a);
     else
         kernel<<<grid, block, 0, s>>>(a);
@@ -455,9 +455,33 @@ __device__ __forceinline__ void merge_group(__amdgpu_buffer_rsrc_t mlr, __amdgpu
     }
 }
 
+// Merge of one query row m of head h over its ncr chunks (one wave), then the row's output.
+template <DType T, int HD>
+__device__ __forceinline__ void merge_row(const AttnArgs &a, int m, int h, int ncr, int lane) {
+    const __amdgpu_buffer_rsrc_t mlr = coherent_rsrc(a.part_ml), por = coherent_rsrc(a.part_o);
+    const size_t slot0 = ((size_t)m * a.n_heads + h) * a.chunk_stride;
+    float Mr = -INFINITY, L = 0.f, o[HD / 64];
+#pragma unroll
+    for (int q = 0; q < HD / 64; ++q) o[q] = 0.f;
+    for (int c0 = 0; c0 < ncr; c0 += 64) {
+        const int cn = min(64, ncr - c0);
+        if (cn <= 8)
+            merge_group<HD, 8>(mlr, por, slot0 + c0, cn, lane, Mr, L, o);
+        else if (cn <= 16)
+            merge_group<HD, 16>(mlr, por, slot0 + c0, cn, lane, Mr, L, o);
+        else if (cn <= 32)
+            merge_group<HD, 32>(mlr, por, slot0 + c0, cn, lane, Mr, L, o);
+        else
+            merge_group<HD, 64>(mlr, por, slot0 + c0, cn, lane, Mr, L, o);
+    }
+#pragma unroll
+    for (int q = 0; q < HD / 64; ++q)
+        St<T>::store(a.O, fm_index<T>(m, h * HD + (HD / 64) * lane + q, a.n_heads * HD), o[q] / L);
+}
+
 constexpr long kAttnPackWaves = 2048;
 
-template <DType T, int HD, int WPB>
+template <DType T, int HD, int WPB, bool MERGE>
 __global__ void __launch_bounds__(64 * WPB) attn_kernel(AttnArgs a) {
     typedef typename St<T>::type E;
     constexpr int KC = (T == DType::BF16) ? 32 : 16;   // reduction depth of one fragment step
@@ -618,6 +642,8 @@ __global__ void __launch_bounds__(64 * WPB) attn_kernel(AttnArgs a) {
         }
     }
 
+    // Without MERGE, attn_merge_kernel merges in a launch of its own and this workgroup is done.
+    if (!MERGE) return;
     // The workgroup that finishes last for (b, kv head) merges every row's chunks.
     __builtin_amdgcn_s_waitcnt(0);  // this workgroup's partial stores have completed
     __syncthreads();
@@ -631,43 +657,42 @@ __global__ void __launch_bounds__(64 * WPB) attn_kernel(AttnArgs a) {
     }
     __syncthreads();
     if (!is_last) return;
-    // Merge, one wave per row.
-    const __amdgpu_buffer_rsrc_t mlr = coherent_rsrc(a.part_ml), por = coherent_rsrc(a.part_o);
     for (int row = w; row < R; row += WPB) {
         const int i = row / G, gi = row - i * G;
-        const int m = b * a.c + i, h = kvh * G + gi;
-        const int ncr = (len0 + i) / CK + 1;
-        const size_t slot0 = ((size_t)m * a.n_heads + h) * a.chunk_stride;
-        float Mr = -INFINITY, L = 0.f, o[HD / 64];
-#pragma unroll
-        for (int q = 0; q < HD / 64; ++q) o[q] = 0.f;
-        for (int c0 = 0; c0 < ncr; c0 += 64) {
-            const int cn = min(64, ncr - c0);
-            if (cn <= 8)
-                merge_group<HD, 8>(mlr, por, slot0 + c0, cn, lane, Mr, L, o);
-            else if (cn <= 16)
-                merge_group<HD, 16>(mlr, por, slot0 + c0, cn, lane, Mr, L, o);
-            else if (cn <= 32)
-                merge_group<HD, 32>(mlr, por, slot0 + c0, cn, lane, Mr, L, o);
-            else
-                merge_group<HD, 64>(mlr, por, slot0 + c0, cn, lane, Mr, L, o);
-        }
-#pragma unroll
-        for (int q = 0; q < HD / 64; ++q)
-            St<T>::store(a.O, fm_index<T>(m, h * HD + (HD / 64) * lane + q, a.n_heads * HD), o[q] / L);
+        merge_row<T, HD>(a, b * a.c + i, kvh * G + gi, (len0 + i) / CK + 1, lane);
     }
+}
+
+// The merge as a launch of its own: one wave per (query row, head), all at once.
+template <DType T, int HD>
+__global__ void __launch_bounds__(256) attn_merge_kernel(AttnArgs a) {
+    const int lane = threadIdx.x & 63;
+    const int gw = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (gw >= a.B * a.c * a.n_heads) return;  // uniform across the wave
+    const int m = gw / a.n_heads, h = gw - m * a.n_heads;
+    const int b = m / a.c, i = m - b * a.c;
+    merge_row<T, HD>(a, m, h, (a.lens[b] + a.pos_off + i) / CK + 1, lane);
 }
 
 template <DType T, int HD>
 static void launch_attention_t(const AttnArgs &a, hipStream_t s, const LaunchEvents &ev) {
     // One wave per 64-key chunk, four chunks per workgroup: the workgroup that finishes last
     // merges with four waves.  A single query row per kv head over a small grid takes one wave
-    // per workgroup instead, which spreads the chunks over more compute units.
+    // per workgroup instead, which spreads the chunks over more compute units.  A large grid
+    // merges in a second launch instead: otherwise every workgroup would wait for its partial
+    // stores before counting itself done, and the last merges would run at the kernel's tail.
     const long waves = (long)a.n_chunks * a.n_kv * a.B;
-    if (a.c * (a.n_heads / a.n_kv) == 1 && waves < kAttnPackWaves) {
-        launch_timed(attn_kernel<T, HD, 1>, dim3(a.n_chunks, a.n_kv, a.B), dim3(64), s, ev, a);
+    if (waves >= kAttnPackWaves) {
+        const int rows = a.B * a.c * a.n_heads;
+        LaunchEvents e1 = ev, e2 = ev;  // one interval around both launches
+        e1.stop = nullptr;
+        e2.start = nullptr;
+        launch_timed(attn_kernel<T, HD, 4, false>, dim3((a.n_chunks + 3) / 4, a.n_kv, a.B), dim3(256), s, e1, a);
+        launch_timed(attn_merge_kernel<T, HD>, dim3((rows + 3) / 4), dim3(256), s, e2, a);
+    } else if (a.c * (a.n_heads / a.n_kv) == 1) {
+        launch_timed(attn_kernel<T, HD, 1, true>, dim3(a.n_chunks, a.n_kv, a.B), dim3(64), s, ev, a);
     } else {
-        launch_timed(attn_kernel<T, HD, 4>, dim3((a.n_chunks + 3) / 4, a.n_kv, a.B), dim3(256), s, ev, a);
+        launch_timed(attn_kernel<T, HD, 4, true>, dim3((a.n_chunks + 3) / 4, a.n_kv, a.B), dim3(256), s, ev, a);
     }
 }
 

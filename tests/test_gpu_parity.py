@@ -242,22 +242,26 @@ def test_drafter_update_objective_variants(obj):
     eng.close()
 
 
-def test_batched_sequences_are_independent():
-    """Batch of 4 equals four single-sequence runs, token for token and bitwise in KV."""
+@pytest.mark.parametrize("P", [40, 1000])
+def test_batched_sequences_are_independent(P):
+    """Batch of 4 equals four single-sequence runs, token for token and bitwise in KV.  With
+    1000-token prompts the batch's attention grid is large enough to merge in a launch of its
+    own, while the single sequences merge inside the attention kernel: both give the same bits."""
     shape = gu.SHAPES["7b_L4"]
-    P, T, B = 40, 20, 4
+    T, B = 20, 4
     prompts = synth.make_prompts(shape.vocab, B, P, 9)
     w = synth.make_weights(shape, 0)
     eng, _ = gu.engine(shape, max_batch=B, max_seq=P + T + 16, weights=w)
     toks, info = eng.generate(prompts, T, 4)
-    kvb = [eng.read_kv(1, b, 0, P + 5) for b in range(B)]
+    kvb = {l: [eng.read_kv(l, b, 0, P + 5) for b in range(B)] for l in (1, shape.n_layers - 1)}
     eng.close()
     eng1, _ = gu.engine(shape, max_batch=1, max_seq=P + T + 16, weights=w)
     for b in range(B):
         t1, _ = eng1.generate(prompts[b:b + 1], T, 4)
         assert np.array_equal(t1[0], toks[b]), b
-        k, v = eng1.read_kv(1, 0, 0, P + 5)
-        assert np.array_equal(k, kvb[b][0]) and np.array_equal(v, kvb[b][1])
+        for l, ref in kvb.items():
+            k, v = eng1.read_kv(l, 0, 0, P + 5)
+            assert np.array_equal(k, ref[b][0]) and np.array_equal(v, ref[b][1]), (l, b)
     eng1.close()
 
 
