@@ -261,6 +261,19 @@ dvi_status dvi_probe_kernel(dvi_ctx *ctx, int32_t which);
 dvi_status dvi_probe_read(dvi_ctx *ctx, double *total_ms, int64_t *launches, double *bytes);
 
 /*
+ * Sampled drafting (Section 3.3 writes the draft as a sample t~ ~ p_theta; the default, tau = 0,
+ * takes the argmax).  With tau > 0 every draft of dvi_draft is drawn from softmax(z / tau), z
+ * the draft-head logits, by Gumbel-max: t~ = argmax_v z_v / tau - log(-log(u_v)).  u comes from
+ * Philox4x64-10 (Salmon et al., SC 2011) with key (seed, 0) and counter (v / 4, b * 16 + j,
+ * step, 0): word v % 4 of the block, b the sequence, j the draft index, step the decode steps
+ * committed since the last dvi_prefill; u = (2 * (x >> 41) + 1) / 2^24.  Commits stay
+ * exactly those of greedy decoding: only the drafts, and so the accept lengths, change.
+ * dvi_read_draft_logits still returns z.  Errors: DVI_ERR_ARG for tau < 0 or not finite;
+ * DVI_ERR_STATE during a step.  Drops the cached graphs.
+ */
+dvi_status dvi_set_sampling(dvi_ctx *ctx, float tau, uint64_t seed);
+
+/*
  * Graph replay of the decode passes (DVI's step structure, Section 3.3: a draft of
  * k_spec shallow passes and one block verify).  enable = 1 (the default on a
  * non-null stream): dvi_draft and dvi_verify launch one captured HIP graph per

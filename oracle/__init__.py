@@ -12,6 +12,8 @@ Contents
              output) and the DVI draft/verify/commit/log rollout (Section 3.3)
   update.py  the KL->RL drafter objective, its gradient, Adam and the schedule
              (Section 3.4)
+  sampling.py  seeded stochastic drafting (t~ ~ p_theta, Section 3.3) by
+             Gumbel-max with Philox4x64-10 uniforms
 
 What pins each part (tests/test_oracle_pins.py, tests/test_oracle_update_pins.py):
   layers / heads      a float64 reference assembled from torch.nn.functional
@@ -30,6 +32,9 @@ What pins each part (tests/test_oracle_pins.py, tests/test_oracle_update_pins.py
                       dL/dz = 0; KL = 0 and gradient 0 at z = logits/tau; A_s = 0 =>
                       dB = 0; gamma = 0 => no gradient; torch autograd
   adam_step           torch.optim.Adam
+  sampling            Philox4x64-10 == numpy's Philox bit generator (bit for bit);
+                      sampled drafts follow softmax(z / tau) (chi-square); the rollout
+                      with sampled drafts == greedy_ar (tests/test_oracle_sampling.py)
   Schedule            closed-form values.  The schedule's constants (lambda0,
                       lambda_kl_min, lambda_pg_max, w_rl, T_warmup, T_ramp, EMA rate)
                       are not given in the paper: parity unpinned for those values.

@@ -17,7 +17,8 @@ Readings taken where the text is silent (each listed in the design notes):
   * layers are 1-based in the text; here layer index l in 0..L-1 is text
     layer l+1, so the draft path is 0..k-1 and the target path k..L-1;
   * both heads read RMSNorm(h; g_final);
-  * drafting is greedy (argmax of p_theta), ties to the lowest id;
+  * drafting is greedy (argmax of p_theta), ties to the lowest id, unless the drafter
+    samples (oracle/sampling.py: Gumbel-max over z / tau with Philox4x64-10 noise);
   * when all k_spec drafts agree (m = k_spec) no extra token is produced:
     k_spec tokens are committed and the last one is processed next step, so a
     step commits n = min(m+1, k_spec) tokens;
@@ -31,6 +32,7 @@ from typing import Callable, List, Optional
 import numpy as np
 
 from . import OracleModel, argmax_lowest, top2_gap
+from . import sampling
 
 
 @dataclasses.dataclass
@@ -83,6 +85,7 @@ class StepRecord:
     n: int
     target_logits: np.ndarray  # float64 [k_spec, V]
     target_gaps: np.ndarray    # float64 [k_spec]
+    draft_gaps: Optional[np.ndarray] = None  # float64 [k_spec]: top-2 gap of each draft's scores
 
 
 @dataclasses.dataclass
@@ -106,10 +109,15 @@ def agree_prefix(drafts, targets) -> int:
 
 @dataclasses.dataclass
 class Drafter:
-    """LoRA draft-head parameters theta = {A_s, B_s} and the scale gamma_s."""
+    """LoRA draft-head parameters theta = {A_s, B_s} and the scale gamma_s.  sample_tau > 0
+    draws each draft from softmax(z / sample_tau) with the seeded Gumbel-max of
+    oracle/sampling.py (sequence index seq in the counter); 0 drafts by argmax."""
     A: np.ndarray    # [V, r]
     B: np.ndarray    # [r, d]
     gamma: float
+    sample_tau: float = 0.0
+    seed: int = 0
+    seq: int = 0
 
 
 def dvi_generate(model: OracleModel, prompt, n_new: int, k_spec: int, drafter: Drafter,
@@ -140,12 +148,16 @@ def dvi_generate(model: OracleModel, prompt, n_new: int, k_spec: int, drafter: D
     while len(out) < n_new and (max_steps is None or step < max_steps):
         # ---- draft: k_spec serial single-token passes through layers 1..k
         tau = [out[-1]]
-        hk_rows, drafts = [], []
+        hk_rows, drafts, dgaps = [], [], []
         forced = forced_drafts(step, length, np.array(out, np.int32)) if forced_drafts else None
         for j in range(k_spec):
             hj = model.layers(cache, model.embed([tau[j]]), length + j, 0, k)
             hk_rows.append(hj[0])
             zt = model.draft_logits(model.final_norm(hj), drafter.A, drafter.B, drafter.gamma)
+            if drafter.sample_tau > 0:
+                zt = sampling.sample_scores(zt, drafter.sample_tau, drafter.seed, step,
+                                            drafter.seq * sampling.ROW_STRIDE + j)[None, :]
+            dgaps.append(float(top2_gap(zt)[0]))
             t_next = int(argmax_lowest(zt)[0]) if forced is None else int(forced[j])
             drafts.append(t_next)
             tau.append(t_next)
@@ -166,7 +178,7 @@ def dvi_generate(model: OracleModel, prompt, n_new: int, k_spec: int, drafter: D
             res.buffer.append(BufferRow(hk_hat[i - 1], drafts[i - 1], zl[i - 1],
                                         1 if i <= m else 0, i, tau[i - 1]))
         res.steps.append(StepRecord(length - n, np.array(drafts, np.int32), targets.copy(), m, n,
-                                    zl, top2_gap(zl)))
+                                    zl, top2_gap(zl), np.array(dgaps)))
         res.length = length
         if on_step is not None:
             res.tokens = np.array(out, np.int32)

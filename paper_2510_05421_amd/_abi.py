@@ -64,6 +64,7 @@ SIGNATURES = {
     "dvi_write_buffer": (c_i32, [c_vp, c_i32, c_vp, c_vp, c_vp, c_vp, c_vp]),
     "dvi_get_timings": (c_i32, [c_vp, c_vp, c_vp, c_vp, c_vp]),
     "dvi_set_graphs": (c_i32, [c_vp, c_i32]),
+    "dvi_set_sampling": (c_i32, [c_vp, c_f32, ctypes.c_uint64]),
     "dvi_probe_kernel": (c_i32, [c_vp, c_i32]),
     "dvi_probe_read": (c_i32, [c_vp, c_vp, c_vp, c_vp]),
 }

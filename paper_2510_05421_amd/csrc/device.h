@@ -189,6 +189,28 @@ __device__ __forceinline__ uint4 mask_keys(uint4 v, int first, int limit) {
     return uint4{w[0], w[1], w[2], w[3]};
 }
 
+// Philox4x64-10 (Salmon et al., "Parallel random numbers: as easy as 1, 2, 3", SC 2011): ten
+// rounds of two 64x64 -> 128-bit products on a 4-word counter, the key advanced by the Weyl
+// increments before each round after the first.
+__device__ __forceinline__ void philox4x64_10(uint64_t (&c)[4], uint64_t k0, uint64_t k1) {
+    constexpr uint64_t M0 = 0xD2E7470EE14C6C93ull, M1 = 0xCA5A826395121157ull;
+    constexpr uint64_t W0 = 0x9E3779B97F4A7C15ull, W1 = 0xBB67AE8584CAA73Bull;
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        if (r) {
+            k0 += W0;
+            k1 += W1;
+        }
+        const uint64_t hi0 = __umul64hi(M0, c[0]), lo0 = M0 * c[0];
+        const uint64_t hi1 = __umul64hi(M1, c[2]), lo1 = M1 * c[2];
+        const uint64_t n0 = hi1 ^ c[1] ^ k0, n2 = hi0 ^ c[3] ^ k1;
+        c[0] = n0;
+        c[1] = lo1;
+        c[2] = n2;
+        c[3] = lo0;
+    }
+}
+
 // Operands of a tile's epilogue that do not depend on the product (residual rows and the next
 // norm's gain; positions and rotary (cos, sin)).  The epilogue wave requests them before the
 // weight stream, so the epilogue after it only computes and stores.  Same lane layout as the
@@ -327,6 +349,19 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &a, int nt, const f
         } else {  // EPI_LOGITS
             float best = -INFINITY;
             int bidx = 0x3fffffff, bad = 0;
+            // sampled drafting: Gumbel noise of the lane's four vocabulary entries (one block)
+            float gn[4] = {0.f, 0.f, 0.f, 0.f};
+            const bool sample = a.sample_tau > 0.f;
+            if (sample) {
+                uint64_t c[4] = {(uint64_t)(nt * 4 + G4), (uint64_t)(m * a.rng_row_stride + a.rng_row0),
+                                 (uint64_t)(uint32_t)a.rng_step[0], 0ull};
+                philox4x64_10(c, a.seed, 0ull);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const float u = (float)(2u * (uint32_t)(c[j] >> 41) + 1u) * 0x1p-24f;
+                    gn[j] = -logf(-logf(u));
+                }
+            }
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const int n = nt * 16 + 4 * G4 + j;
@@ -340,8 +375,9 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &a, int nt, const f
                 }
                 if (valid) a.Z[(size_t)m * a.N + n] = y;
                 if (!isfinite(y)) bad = 1;
-                if (y > best) {
-                    best = y;
+                const float score = sample ? y / a.sample_tau + gn[j] : y;
+                if (score > best) {
+                    best = score;
                     bidx = n;
                 }
             }

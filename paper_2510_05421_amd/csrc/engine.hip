@@ -68,6 +68,7 @@ struct dvi_ctx {
     int32_t *part_idx;
     // small device state; io block is one contiguous region copied back at commit
     int32_t *lens, *pending, *drafts, *targets, *forced, *max_new, *ids, *copy_list, *ring_state;
+    int32_t *rng_step;  // [0]: decode steps committed since the prefill (the sampling counter)
     int32_t *io;  // [0,B*k) tokens | [B*k, B*k+B) n | [.., +B) m | flags[4]
     int32_t *prow;
     // replay ring
@@ -89,6 +90,9 @@ struct dvi_ctx {
     bool ev_ok = false;
     float ms[4] = {0, 0, 0, 0};
     int ev_pending[4] = {0, 0, 0, 0};
+    // sampled drafting (0: argmax drafting)
+    float samp_tau = 0.f;
+    uint64_t samp_seed = 0;
     // captured decode passes: (phase, B, k_spec, variant, attention chunks) -> graph
     bool graphs = false;
     std::map<std::array<int, 5>, hipGraphExec_t> gcache;
@@ -189,6 +193,7 @@ static size_t layout(dvi_ctx *x, const dvi_config &c, void *base) {
     int32_t *ids = b.take<int32_t>((size_t)c.max_batch * c.max_seq * 4);
     int32_t *copy_list = b.take<int32_t>((1 + 2 * Bk) * 4);
     int32_t *ring_state = b.take<int32_t>(4 * 4);
+    int32_t *rng_step = b.take<int32_t>(4 * 4);
     int32_t *io = b.take<int32_t>((Bk + 2 * c.max_batch + 4) * 4);
     size_t maxN = V;
     if ((size_t)qkv_rows(c) > maxN) maxN = qkv_rows(c);
@@ -222,7 +227,7 @@ static size_t layout(dvi_ctx *x, const dvi_config &c, void *base) {
         x->lora_u = lora_u;
         x->att_po = att_po; x->att_pml = att_pml; x->att_cnt = att_cnt; x->chunk_stride = (int)cs;
         x->lens = lens; x->pending = pending; x->drafts = drafts; x->targets = targets; x->forced = forced;
-        x->max_new = max_new; x->ids = ids; x->copy_list = copy_list; x->ring_state = ring_state; x->io = io;
+        x->max_new = max_new; x->ids = ids; x->copy_list = copy_list; x->ring_state = ring_state; x->rng_step = rng_step; x->io = io;
         x->prow = prow;
         x->ring_h = ring_h; x->ring_logits = ring_logits; x->ring_a = ring_a; x->ring_i = ring_i;
         x->ring_prev = ring_prev; x->ring_r = ring_r; x->ring_fresh = ring_fresh;
@@ -380,7 +385,7 @@ extern "C" dvi_status dvi_create(const dvi_config *cfg, const dvi_weights *w, vo
         const size_t R = c.buffer_rows, r = c.lora_rank;
         struct Z { void *p; size_t n; } zs[] = {
             {x->lens, (size_t)c.max_batch * 4}, {x->pending, (size_t)c.max_batch * 4}, {x->drafts, Bk * 4},
-            {x->targets, Bk * 4}, {x->io, (Bk + 2 * (size_t)c.max_batch + 4) * 4}, {x->ring_state, 16},
+            {x->targets, Bk * 4}, {x->io, (Bk + 2 * (size_t)c.max_batch + 4) * 4}, {x->ring_state, 16}, {x->rng_step, 16},
             {x->ring_fresh, R}, {x->ring_r, R}, {x->mA, (size_t)V * r * 4}, {x->vA, (size_t)V * r * 4},
             {x->mB, r * d * 4}, {x->vB, r * d * 4}, {x->att_cnt, (size_t)c.max_batch * c.n_kv_heads * 4}};
         for (const Z &z : zs)
@@ -478,6 +483,8 @@ static const float *next_gain(dvi_ctx *x, int l) {
 // Attention grid of a call whose rows reach at most position pmax: its 64-key chunks rounded up
 // to a multiple of 4 (a 256-position bucket), so that a captured pass stays valid until the
 // longest sequence crosses a bucket edge.  Workgroups past a sequence's own chunks exit at once.
+constexpr int kSampleRowStride = 16;  // counter row = sequence * 16 + draft index (k_spec <= 16)
+
 static int attn_chunks(const dvi_ctx *x, int pmax) {
     const int n = (pmax / 64 + 1 + 3) / 4 * 4;
     return n < x->chunk_stride ? n : x->chunk_stride;
@@ -577,10 +584,18 @@ static int32_t *flags_ptr(dvi_ctx *x) { return x->io + io_flags(x); }
 
 // Vocabulary head on M rows of X (FM): logits -> Z, argmax -> out (stride).
 // ss_in != nullptr: X holds dtype(h * final_norm) and rows are scaled by 1/rms (folded norm).
+// draft_j >= 0: the draft head of draft index j, sampled when sampling is on.
 static void head(dvi_ctx *x, const void *X, const float *ss_in, int ld_ss, int M, float *Z, bool lora, int32_t *out,
-                 int out_stride, const int32_t *forced) {
+                 int out_stride, const int32_t *forced, int draft_j = -1) {
     const dvi_config &cf = x->cfg;
     GemmArgs a{};
+    if (draft_j >= 0 && x->samp_tau > 0.f) {
+        a.sample_tau = x->samp_tau;
+        a.seed = x->samp_seed;
+        a.rng_step = x->rng_step;
+        a.rng_row0 = draft_j;
+        a.rng_row_stride = kSampleRowStride;
+    }
     a.ss_in = ss_in;
     a.ld_ss_in = ld_ss;
     a.eps = cf.rms_eps;
@@ -636,6 +651,16 @@ static dvi_status run_pass(dvi_ctx *x, const std::array<int, 5> &key, Body &&bod
     return DVI_OK;
 }
 
+extern "C" dvi_status dvi_set_sampling(dvi_ctx *x, float tau, uint64_t seed) {
+    if (!x) return DVI_ERR_ARG;
+    if (!(tau >= 0.f) || !isfinite(tau)) return fail(x, DVI_ERR_ARG, "sampling temperature must be finite and >= 0");
+    if (x->state == S_DRAFTED || x->state == S_VERIFIED) return fail(x, DVI_ERR_STATE, "sampling set during a step");
+    x->samp_tau = tau;
+    x->samp_seed = seed;
+    drop_graphs(x);  // the draft head's arguments changed
+    return DVI_OK;
+}
+
 extern "C" dvi_status dvi_set_graphs(dvi_ctx *x, int32_t enable) {
     if (!x) return DVI_ERR_ARG;
     if (enable && x->stream == nullptr) return fail(x, DVI_ERR_ARG, "graphs need a stream other than the null stream");
@@ -671,6 +696,7 @@ extern "C" dvi_status dvi_prefill(dvi_ctx *x, int32_t batch, const int32_t *ids,
     const int d = cf.d_model;
     HIPCHK(x, hipMemcpyAsync(x->ids, packed.data(), packed.size() * 4, hipMemcpyHostToDevice, x->stream));
     HIPCHK(x, hipMemsetAsync(x->lens, 0, cf.max_batch * 4, x->stream));
+    HIPCHK(x, hipMemsetAsync(x->rng_step, 0, 4, x->stream));
     HIPCHK(x, hipMemsetAsync(flags_ptr(x), 0, 16, x->stream));
     x->B = batch;
     for (int b = 0; b < cf.max_batch; ++b) x->lens_h[b] = 0;
@@ -741,7 +767,7 @@ extern "C" dvi_status dvi_draft(dvi_ctx *x, int32_t k_spec, const int32_t *force
                 launch_head_prep(x->dt, h, k_spec * d, ss, k_spec * nps, x->final_norm, B, d, cf.rms_eps, x->lora_B,
                                  cf.lora_rank, xh, k_spec * d, x->dfm, x->lora_u, x->stream);
                 head(x, x->dfm, nullptr, 0, B, x->dlogits, true, x->drafts + j, k_spec,
-                     forced ? x->forced + j : nullptr);
+                     forced ? x->forced + j : nullptr, j);
             }
         }
         LAUNCHCHK(x);
@@ -838,6 +864,7 @@ extern "C" dvi_status dvi_commit(dvi_ctx *x, const int32_t *max_new, const int32
     a.ring_prev = x->ring_prev;
     a.ring_r = x->ring_r;
     a.ring_fresh = x->ring_fresh;
+    a.rng_step = x->rng_step;
     if (x->ar_mode) {
         // plain autoregressive step: nothing was drafted; commit y*_1 only
         HIPCHK(x, hipMemsetAsync(x->drafts, 0xff, (size_t)B * 4, x->stream));

@@ -69,6 +69,13 @@ struct GemmArgs {
     float gamma;
     float *part_val;    // [M][N/16]
     int32_t *part_idx;  // [M][N/16]
+    // Sampled drafting (EPI_LOGITS): when sample_tau > 0 the argmax partials rank
+    // z / sample_tau + g, g = -log(-log(u)), u from Philox4x64-10 with key (seed, 0) and counter
+    // (n / 4, m * rng_row_stride + rng_row0, *rng_step, 0); Z keeps z itself.
+    float sample_tau;
+    uint64_t seed;
+    const int32_t *rng_step;
+    int rng_row0, rng_row_stride;
 };
 // Optional start/stop events for one launch: when set, the kernel is launched with
 // hipExtLaunchKernelGGL, which stamps the events at the kernel's own start and end (the same
@@ -137,6 +144,7 @@ struct CommitArgs {
     int32_t *copy_list;       // [B*k_spec][2]: (source row b*k_spec+i-1, ring slot), count at [-1]
     int32_t *ring_a, *ring_i, *ring_prev;
     int8_t *ring_r, *ring_fresh;
+    int32_t *rng_step;        // [0]: decode steps committed since the prefill (sampling counter)
 };
 void launch_commit(const CommitArgs &a, hipStream_t s);
 

@@ -812,6 +812,7 @@ __global__ void commit_kernel(CommitArgs a) {
     a.copy_list[0] = cnt;
     a.ring_state[0] = next;
     a.ring_state[1] = valid;
+    a.rng_step[0] += 1;
 }
 
 void launch_commit(const CommitArgs &a, hipStream_t s) { commit_kernel<<<1, 64, 0, s>>>(a); }

@@ -141,6 +141,11 @@ class Engine:
             self.lib.dvi_destroy(self.ctx)
             self.ctx = None
 
+    def set_sampling(self, tau: float, seed: int = 0):
+        """Draw every draft from softmax(z / tau) with seeded Gumbel-max noise (tau = 0: argmax
+        drafting, the default).  Commits are unchanged: they are greedy decoding's."""
+        self._check(self.lib.dvi_set_sampling(self.ctx, float(tau), int(seed) & 0xFFFFFFFFFFFFFFFF))
+
     def set_graphs(self, enable: bool):
         """Replay the draft and verify passes as captured HIP graphs (the default) or launch
         every kernel directly; results are bitwise the same."""

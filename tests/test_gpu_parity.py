@@ -328,7 +328,8 @@ def test_state_capacity_and_numeric_errors():
     eng.close()
 
 
-def test_graph_replay_equals_direct_launches():
+@pytest.mark.parametrize("tau", [0.0, 1.0])
+def test_graph_replay_equals_direct_launches(tau):
     """Draft and verify replayed from captured HIP graphs give the tokens, accept lengths, keys,
     values and drafter updates of direct launches, bitwise.  The prompts end just before a
     256-position attention-grid bucket edge, so generation re-captures there; drafter updates,
@@ -341,6 +342,7 @@ def test_graph_replay_equals_direct_launches():
     for graphs in (True, False):
         eng, _ = gu.engine(shape, max_batch=B, max_seq=P + T + 16, weights=w)
         eng.set_graphs(graphs)
+        eng.set_sampling(tau, 5)
         toks, info = eng.generate(prompts, T, 4, update_every=3)
         ar, _ = eng.generate(prompts, 12, 1)
         lens = eng.lengths().copy()
@@ -358,3 +360,64 @@ def test_graph_replay_equals_direct_launches():
     assert np.array_equal(lg[0], ld[0]) and np.array_equal(lg[1], ld[1])
     for a, b in zip(ig["updates"], id_["updates"]):
         assert a["loss"] == b["loss"] and a["rows"] == b["rows"]
+
+
+@pytest.mark.parametrize("name,tau", [("tiny", 1.0), ("tiny", 0.5), ("1b_L4", 1.0)])
+def test_sampled_drafts_match_oracle(name, tau):
+    """Seeded stochastic drafting: each draft is the oracle's Gumbel-max draw (same generator,
+    seed, step and row) wherever the oracle's perturbed scores are not near a tie; commits stay
+    greedy decoding's."""
+    shape = gu.SHAPES[name]
+    k = KSPEC[name]
+    P, T, seed = 24, 40, 11
+    w = synth.make_weights(shape, 0, lora_A_std=0.05)
+    prompt = synth.make_prompts(shape.vocab, 1, P, 5)[0]
+    drafter = odvi.Drafter(w.lora_A.astype(np.float64), w.lora_B.astype(np.float64), shape.lora_gamma,
+                           sample_tau=tau, seed=seed)
+    om = oracle.OracleModel(w)
+    ref = odvi.dvi_generate(om, prompt, T, k, drafter)
+    ar = odvi.greedy_ar(om, prompt, T)
+    assert np.array_equal(ref.tokens, ar.tokens)
+    eng, _ = gu.engine(shape, max_seq=P + T + 16, weights=w)
+    eng.set_sampling(tau, seed)
+    toks, steps = _gpu_run(eng, prompt, T, k)
+    agree, differ = 0, 0
+    for st, (d, tg, m, n) in zip(ref.steps, steps):
+        ok = True
+        for j in range(k):
+            if st.draft_gaps[j] <= 1e-3:     # a near-tie of the perturbed scores: either draw
+                ok = False
+                break
+            assert d[j] == st.drafts[j], "step drafts %s != oracle %s" % (d, st.drafts)
+            agree += 1
+        if not ok:
+            break
+        assert m == st.m and n == st.n
+        differ += int(not np.array_equal(st.drafts, st.targets))
+    _say("sampled %s tau=%g: %d drafts agree with the oracle before the first near-tie" % (name, tau, agree))
+    assert agree >= 2 * k
+    gu.compare_free_running(toks, ar.tokens, ar.gaps)
+    eng.close()
+
+
+def test_sampled_drafting_is_lossless_and_changes_drafts():
+    """With sampled drafts, speculative decoding still equals greedy decoding bitwise (tokens
+    and keys/values); the accept lengths differ from argmax drafting."""
+    shape = gu.SHAPES["7b_L4"]
+    P, T, B = 60, 48, 2
+    prompts = synth.make_prompts(shape.vocab, B, P, 31)
+    w = synth.make_weights(shape, 0, lora_A_std=0.02)
+    eng, _ = gu.engine(shape, max_batch=B, max_seq=P + T + 16, weights=w)
+    greedy_tok, greedy_info = eng.generate(prompts, T, 4)
+    eng.set_sampling(1.0, 99)
+    samp_tok, samp_info = eng.generate(prompts, T, 4)
+    kv_s = [eng.read_kv(l, b, 0, P + T - 1) for l in (1, 3) for b in range(B)]
+    eng.set_sampling(0.0)
+    ar_tok, _ = eng.generate(prompts, T, 1)
+    kv_a = [eng.read_kv(l, b, 0, P + T - 1) for l in (1, 3) for b in range(B)]
+    assert np.array_equal(samp_tok, ar_tok) and np.array_equal(greedy_tok, ar_tok)
+    for (k1, v1), (k2, v2) in zip(kv_s, kv_a):
+        assert np.array_equal(k1, k2) and np.array_equal(v1, v2)
+    _say("sampled drafting: mean m %.2f vs argmax drafting %.2f" % (samp_info["m"].mean(), greedy_info["m"].mean()))
+    assert samp_info["steps"] != greedy_info["steps"] or not np.array_equal(samp_info["m"], greedy_info["m"])
+    eng.close()
