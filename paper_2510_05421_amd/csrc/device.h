@@ -222,14 +222,15 @@ struct EpiOperands {
     int pos[MG];     // QKV: position of the token
 };
 
-// Stage 1: everything but the rotary table, whose address needs the position.
+// Stage 1: everything but the rotary table, whose address needs the position.  m0: token of
+// the first row group.
 template <int MG, int EPI>
-__device__ __forceinline__ void epilogue_prefetch(const GemmArgs &a, int nt, EpiOperands<MG> &e) {
+__device__ __forceinline__ void epilogue_prefetch(const GemmArgs &a, int nt, EpiOperands<MG> &e, int m0 = 0) {
     const int lane = threadIdx.x & 63;
     const int G4 = lane >> 4;
 #pragma unroll
     for (int g = 0; g < MG; ++g) {
-        const int m = 16 * g + (lane & 15);
+        const int m = m0 + 16 * g + (lane & 15);
         const int row = m < a.M ? m : 0;  // rows past M read row 0 and are never used
         if (EPI == EPI_RESID) {
             const float4 h4 = *(const float4 *)(a.H + (size_t)row * a.ldh + nt * 16 + 4 * G4);
@@ -269,20 +270,21 @@ __device__ __forceinline__ void epilogue_prefetch_rope(const GemmArgs &a, int nt
         }
 }
 
-// Epilogue of one 16-feature output tile nt (rows of the weight matrix) for all M tokens,
-// run by the wave that holds the tile's reduced sums (mine[g]: MFMA output layout, lane l holds
-// features nt*16 + 4*(l/16) + j of token 16*g + l%16) and the tile's prefetched operands e.
-// sinv holds 1/rms per token when the input was pre-scaled by the norm gain (folded RMSNorm).
+// Epilogue of one 16-feature output tile nt (rows of the weight matrix) for MG row groups of
+// tokens from m0 on, run by the wave that holds the tile's reduced sums (mine[g]: MFMA output
+// layout, lane l holds features nt*16 + 4*(l/16) + j of token m0 + 16*g + l%16) and the tile's
+// prefetched operands e.  sinv[16*g + l%16] holds 1/rms of that token when the input was
+// pre-scaled by the norm gain (folded RMSNorm).
 template <DType T, int MG, int EPI>
 __device__ __forceinline__ void gemm_epilogue(const GemmArgs &a, int nt, const f32x4 (&mine)[MG], const float *sinv,
-                                              const EpiOperands<MG> &e) {
+                                              const EpiOperands<MG> &e, int m0 = 0) {
     const int lane = threadIdx.x & 63;
     const int G4 = lane >> 4;
 #pragma unroll
     for (int g = 0; g < MG; ++g) {
-        const int m = 16 * g + (lane & 15);
+        const int m = m0 + 16 * g + (lane & 15);
         const bool valid = m < a.M;
-        const float sc = (a.ss_in != nullptr && valid) ? sinv[m] : 1.0f;
+        const float sc = (a.ss_in != nullptr && valid) ? sinv[16 * g + (lane & 15)] : 1.0f;
         f32x4 v = mine[g];
         if (EPI == EPI_RESID) {
             float hv[4] = {0.f, 0.f, 0.f, 0.f};

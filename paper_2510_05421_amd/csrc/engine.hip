@@ -62,6 +62,7 @@ struct dvi_ctx {
     // drafted rows of every sequence (row b*k_spec + j), which the verify then continues.
     // GEMM inputs (hg, act, attn_o, hk_hg, dfm, pfm, ufm) are in the fragment-major layout.
     float *h, *ss, *q, *hk, *hk_ss, *vlogits, *dlogits, *part_val, *lora_u, *att_po, *att_pml;
+    float *sinv_rows;  // 1/rms per token for prefill-block GEMMs
     int32_t *att_cnt;
     int chunk_stride = 0;
     void *hg, *attn_o, *act, *hk_hg, *hk_hat, *dfm, *pfm, *ufm;
@@ -125,6 +126,7 @@ static dvi_status fail(dvi_ctx *c, dvi_status s, const char *fmt, ...) {
     do {                                                                                            \
         hipError_t e_ = hipGetLastError();                                                          \
         if (e_ != hipSuccess) return fail(ctx, DVI_ERR_DEVICE, "kernel launch: %s", hipGetErrorString(e_)); \
+        if ((ctx)->device_error) return DVI_ERR_DEVICE;                                             \
     } while (0)
 
 static size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -135,6 +137,15 @@ static int m_max(const dvi_config &c) {
     int m = c.max_batch * c.max_k_spec;
     return m > kMaxRows ? m : kMaxRows;
 }
+// Rows of one prefill block (batch x prompt positions): up to 2048, fewer when the attention
+// partials of that many rows would pass 2 GiB (they grow with max_seq).
+static int prefill_rows(const dvi_config &c) {
+    const size_t per_row = (size_t)c.n_heads * (((size_t)c.max_seq + 63) / 64) * (c.head_dim + 2) * 4;
+    size_t m = ((size_t)2 << 30) / per_row / 64 * 64;
+    if (m > 2048) m = 2048;
+    const int mm = m_max(c);
+    return (int)m > mm ? (int)m : mm;
+}
 
 // Lay out (or size, when base == nullptr) everything the context keeps on the device.
 static size_t layout(dvi_ctx *x, const dvi_config &c, void *base) {
@@ -142,7 +153,7 @@ static size_t layout(dvi_ctx *x, const dvi_config &c, void *base) {
     const size_t es = c.dtype == DVI_BF16 ? 2 : 4;
     const size_t d = c.d_model, F = c.ffn_dim, V = c.vocab, qd = (size_t)c.n_heads * c.head_dim;
     const size_t kvd = (size_t)c.n_kv_heads * c.head_dim;
-    const size_t M = m_max(c), R = c.buffer_rows, r = c.lora_rank;
+    const size_t M = m_max(c), Mp = prefill_rows(c), R = c.buffer_rows, r = c.lora_rank;
     const size_t cs = ((size_t)c.max_seq + 63) / 64;
     const size_t Bk = (size_t)c.max_batch * c.max_k_spec;
     const size_t cache = (size_t)c.max_batch * kvd * cache_cap(c) * es;
@@ -162,13 +173,15 @@ static size_t layout(dvi_ctx *x, const dvi_config &c, void *base) {
     float *final_norm = b.take<float>(d * 4);
     float2 *rope = b.take<float2>((size_t)c.max_seq * (c.head_dim / 2) * 8);
     const size_t nps = d / 16;
-    const size_t M16 = (M + 15) / 16 * 16, Bk16 = (Bk + 15) / 16 * 16, B16 = ((size_t)c.max_batch + 15) / 16 * 16;
-    float *h = b.take<float>(M * d * 4);
-    float *ss = b.take<float>(M * nps * 4);
-    void *hg = b.take<void>(M16 * d * es);
-    float *q = b.take<float>(M * qd * 4);
-    void *attn_o = b.take<void>(M16 * qd * es);
-    void *act = b.take<void>(M16 * F * es);
+    // activations of a GEMM call: decode steps (M rows) and prefill blocks (Mp >= M rows)
+    const size_t Mp16 = (Mp + 15) / 16 * 16, Bk16 = (Bk + 15) / 16 * 16, B16 = ((size_t)c.max_batch + 15) / 16 * 16;
+    float *h = b.take<float>(Mp * d * 4);
+    float *ss = b.take<float>(Mp * nps * 4);
+    void *hg = b.take<void>(Mp16 * d * es);
+    float *q = b.take<float>(Mp * qd * 4);
+    void *attn_o = b.take<void>(Mp16 * qd * es);
+    void *act = b.take<void>(Mp16 * F * es);
+    float *sinv_rows = b.take<float>(Mp * 4);
     float *hk = b.take<float>(Bk * d * 4);
     float *hk_ss = b.take<float>(Bk * nps * 4);
     void *hk_hg = b.take<void>(Bk16 * d * es);
@@ -181,8 +194,8 @@ static size_t layout(dvi_ctx *x, const dvi_config &c, void *base) {
     float *part_val = b.take<float>(M * (V / 16) * 4);
     int32_t *part_idx = b.take<int32_t>(M * (V / 16) * 4);
     float *lora_u = b.take<float>((M > R ? M : R) * r * 4);
-    float *att_po = b.take<float>(M * c.n_heads * cs * c.head_dim * 4);
-    float *att_pml = b.take<float>(M * c.n_heads * cs * 2 * 4);
+    float *att_po = b.take<float>(Mp * c.n_heads * cs * c.head_dim * 4);
+    float *att_pml = b.take<float>(Mp * c.n_heads * cs * 2 * 4);
     int32_t *att_cnt = b.take<int32_t>((size_t)c.max_batch * c.n_kv_heads * 4);
     int32_t *lens = b.take<int32_t>(c.max_batch * 4);
     int32_t *pending = b.take<int32_t>(c.max_batch * 4);
@@ -220,7 +233,7 @@ static size_t layout(dvi_ctx *x, const dvi_config &c, void *base) {
     if (x && base) {
         x->L = Ls;
         x->emb = emb; x->head = head; x->final_norm = final_norm; x->rope = rope;
-        x->h = h; x->ss = ss; x->hg = hg; x->q = q; x->attn_o = attn_o; x->act = act;
+        x->h = h; x->ss = ss; x->hg = hg; x->q = q; x->attn_o = attn_o; x->act = act; x->sinv_rows = sinv_rows;
         x->hk = hk; x->hk_ss = hk_ss; x->hk_hg = hk_hg; x->hk_hat = hk_hat;
         x->dfm = dfm; x->pfm = pfm; x->ufm = ufm;
         x->vlogits = vlogits; x->dlogits = dlogits; x->part_val = part_val; x->part_idx = part_idx;
@@ -466,8 +479,10 @@ static void gemm(dvi_ctx *x, Epi e, int cls, const void *W, const void *X, int M
     a.M = M;
     a.N = N;
     a.K = K;
+    a.sinv_rows = x->sinv_rows;
     const LaunchEvents ev = probe_begin(x, cls);
-    launch_gemm(x->dt, e, a, x->stream, ev);
+    if (!launch_gemm(x->dt, e, a, x->stream, ev))
+        (void)fail(x, DVI_ERR_DEVICE, "no GEMM variant for %d rows of epilogue %d", M, (int)e);
     probe_end(x, ev, gemm_bytes(x, e, M, N, K));
 }
 
@@ -497,7 +512,7 @@ static int max_len(const dvi_ctx *x) {
 }
 
 static dvi_status run_layers(dvi_ctx *x, int l0, int l1, int B, int c, int pos_off, int n_chunks, float *h, float *ss,
-                             void *hg, int rs, void *out_hg, int out_rs, int out_off) {
+                             void *hg, int rs, void *out_hg, int out_rs, int out_off, bool prefill = false) {
     const dvi_config &cf = x->cfg;
     const int d = cf.d_model, F = cf.ffn_dim, H = cf.n_heads, Hkv = cf.n_kv_heads, hd = cf.head_dim;
     const int nps = d / 16;
@@ -505,6 +520,7 @@ static dvi_status run_layers(dvi_ctx *x, int l0, int l1, int B, int c, int pos_o
     for (int l = l0; l < l1; ++l) {
         const LayerW &Lw = x->L[l];
         GemmArgs a{};
+        a.large_m = prefill;
         a.ss_in = ss;
         a.ld_ss_in = rs * nps;
         a.eps = cf.rms_eps;
@@ -548,6 +564,7 @@ static dvi_status run_layers(dvi_ctx *x, int l0, int l1, int B, int c, int pos_o
             probe_end(x, ev, kv + (double)M * H * hd * (4.0 + x->es));
         }
         GemmArgs r{};
+        r.large_m = prefill;
         r.H = h;
         r.ldh = rs * d;
         r.ss_out = ss;
@@ -558,6 +575,7 @@ static dvi_status run_layers(dvi_ctx *x, int l0, int l1, int B, int c, int pos_o
         r.g_next = Lw.mlp_norm;
         gemm(x, EPI_RESID, DVI_PROBE_ATTN_OUT, Lw.wo, x->attn_o, M, d, H * hd, r);
         GemmArgs g{};
+        g.large_m = prefill;
         g.ss_in = ss;
         g.ld_ss_in = rs * nps;
         g.eps = cf.rms_eps;
@@ -700,14 +718,15 @@ extern "C" dvi_status dvi_prefill(dvi_ctx *x, int32_t batch, const int32_t *ids,
     HIPCHK(x, hipMemsetAsync(flags_ptr(x), 0, 16, x->stream));
     x->B = batch;
     for (int b = 0; b < cf.max_batch; ++b) x->lens_h[b] = 0;
-    const int c = (kMaxRows / batch) < 1 ? 1 : kMaxRows / batch;
+    const int c = (prefill_rows(cf) / batch) < 1 ? 1 : prefill_rows(cf) / batch;  // positions per block
     const int nps = d / 16;
     for (int s0 = 0; s0 < P; s0 += c) {
         const int cc = (P - s0) < c ? P - s0 : c;
         launch_embed(x->dt, x->emb, x->ids + s0, P, batch, cc, d, x->h, d, x->ss, nps, x->hg, x->L[0].attn_norm,
                      x->stream);
         dvi_status st =
-            run_layers(x, 0, cf.n_layers, batch, cc, s0, attn_chunks(x, s0 + cc - 1), x->h, x->ss, x->hg, 1, x->hg, 1, 0);
+            run_layers(x, 0, cf.n_layers, batch, cc, s0, attn_chunks(x, s0 + cc - 1), x->h, x->ss, x->hg, 1, x->hg, 1, 0,
+                       true);
         if (st != DVI_OK) return st;
         if (s0 + cc == P) {  // last prompt token of every sequence -> first generated token
             launch_gather_fm(x->dt, x->hg, true, cc, cc - 1, batch, d, x->pfm, x->stream);

@@ -69,6 +69,11 @@ struct GemmArgs {
     float gamma;
     float *part_val;    // [M][N/16]
     int32_t *part_idx;  // [M][N/16]
+    // Large-M GEMM: taken for M > 64, and for any M when large_m is set (every prefill block,
+    // so a prompt's arithmetic never depends on the batch); sinv_rows is its scratch for 1/rms
+    // of every token [M]
+    int large_m;
+    float *sinv_rows;
     // Sampled drafting (EPI_LOGITS): when sample_tau > 0 the argmax partials rank
     // z / sample_tau + g, g = -log(-log(u)), u from Philox4x64-10 with key (seed, 0) and counter
     // (n / 4, m * rng_row_stride + rng_row0, *rng_step, 0); Z keeps z itself.
@@ -84,7 +89,10 @@ struct LaunchEvents {
     hipEvent_t start = nullptr, stop = nullptr;
 };
 
-void launch_gemm(DType t, Epi e, const GemmArgs &a, hipStream_t s, const LaunchEvents &ev = {});
+// M <= 64: the weight-streaming decode GEMM.  M > 64 or large_m (prefill blocks): the large-M
+// GEMM, which needs sinv_rows when ss_in is set and takes every epilogue but EPI_LOGITS
+// (returns false).  Each kernel's arithmetic per output is independent of M.
+bool launch_gemm(DType t, Epi e, const GemmArgs &a, hipStream_t s, const LaunchEvents &ev = {});
 
 // Row m = b*c + i: h = E[tok[b*tok_stride + i]] (fp32, row stride ldh), its per-16-column
 // sums of squares (ss, stride ld_ss) and dtype(h * g) (hg, FM, row m).

@@ -170,6 +170,93 @@ __global__ void __launch_bounds__(64 * WMAX) gemm_kernel(GemmArgs a) {
     gemm_epilogue<T, MG, EPI>(a, nt, mine, sinv, pre);
 }
 
+// ------------------------------------------------------------------------------------------
+// Large-M GEMM (the prefill: M = batch x prompt block, up to a few thousand tokens).
+//
+// A workgroup of four waves computes 128 tokens x 128 features; wave (wy, wx) owns tokens
+// 64 wy .. +63 (four 16-token groups) and features 64 wx .. +63 (four tiles).  Both operands
+// are fragment-major in memory, so each 16-byte load per lane is an MFMA operand as it stands:
+// per K step a wave loads four weight and four activation fragments and issues 16 MFMAs, two
+// steps in flight.  Workgroups that share a weight block are adjacent in the grid (tokens
+// fastest), so a block leaves HBM about once per XCD.  Fragments past M or N load a valid
+// address and enter as zeros: every MFMA runs unconditionally.  The epilogue is the decode
+// GEMM's, per tile, at the wave's token offset; 1/rms of each token comes from rms_rows_kernel.
+// ------------------------------------------------------------------------------------------
+__global__ void __launch_bounds__(256) rms_rows_kernel(const float *ss, int ld_ss, int nparts, int K, float eps,
+                                                       int M, float *out) {
+    const int m = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (m >= M) return;  // uniform across the wave
+    const float v = inv_rms(ss + (size_t)m * ld_ss, nparts, K, eps);
+    if ((threadIdx.x & 63) == 0) out[m] = v;
+}
+
+template <DType T, int EPI>
+__global__ void __launch_bounds__(256) gemm_big_kernel(GemmArgs a) {
+    constexpr int TG = 4, TF = 4, U = 2;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wy = wave >> 1, wx = wave & 1;
+    const int KC = (T == DType::BF16) ? 32 : 16;
+    const int KT = a.K / KC, NT = a.N / 16, NG = (a.M + 15) / 16;
+    const int g0 = blockIdx.x * 8 + TG * wy, t0 = blockIdx.y * 8 + TF * wx;
+    const uint4 *Wp = (const uint4 *)a.W + lane, *Xp = (const uint4 *)a.X + lane;
+    const uint4 zero = {0u, 0u, 0u, 0u};
+    f32x4 acc[TF][TG];
+#pragma unroll
+    for (int t = 0; t < TF; ++t)
+#pragma unroll
+        for (int g = 0; g < TG; ++g) acc[t][g] = (f32x4){0.f, 0.f, 0.f, 0.f};
+    uint4 wf[U][TF], xf[U][TG];
+    auto fetch = [&](int sl, int k) {
+        const int kc = min(k, KT - 1);
+#pragma unroll
+        for (int t = 0; t < TF; ++t) {
+            const uint4 v = Wp[((size_t)min(t0 + t, NT - 1) * KT + kc) * 64];
+            wf[sl][t] = (k < KT && t0 + t < NT) ? v : zero;
+        }
+#pragma unroll
+        for (int g = 0; g < TG; ++g) {
+            const uint4 v = Xp[((size_t)min(g0 + g, NG - 1) * KT + kc) * 64];
+            xf[sl][g] = (k < KT && g0 + g < NG) ? v : zero;
+        }
+    };
+#pragma unroll
+    for (int sl = 0; sl < U; ++sl) fetch(sl, sl);
+    for (int k0 = 0; k0 < KT; k0 += U) {
+#pragma unroll
+        for (int sl = 0; sl < U; ++sl) {
+#pragma unroll
+            for (int t = 0; t < TF; ++t)
+#pragma unroll
+                for (int g = 0; g < TG; ++g) acc[t][g] = St<T>::mma(wf[sl][t], xf[sl][g], acc[t][g]);
+            fetch(sl, k0 + sl + U);
+        }
+    }
+    if (g0 >= NG) return;  // uniform across the wave
+    const int m0 = 16 * g0;
+#pragma unroll
+    for (int t = 0; t < TF; ++t) {
+        const int nt = t0 + t;
+        if (nt >= NT) break;  // uniform
+        EpiOperands<TG> pre;
+        epilogue_prefetch<TG, EPI>(a, nt, pre, m0);
+        epilogue_prefetch_rope<TG, EPI>(a, nt, pre);
+        gemm_epilogue<T, TG, EPI>(a, nt, acc[t], a.sinv_rows + m0, pre, m0);
+    }
+}
+
+template <DType T>
+static void launch_gemm_big(Epi e, const GemmArgs &a, hipStream_t s, const LaunchEvents &ev) {
+    if (a.ss_in != nullptr)
+        rms_rows_kernel<<<(a.M + 3) / 4, 256, 0, s>>>(a.ss_in, a.ld_ss_in, a.K / 16, a.K, a.eps, a.M, a.sinv_rows);
+    const dim3 grid((a.M + 127) / 128, (a.N / 16 + 7) / 8);
+    switch (e) {
+        case EPI_RESID: launch_timed(gemm_big_kernel<T, EPI_RESID>, grid, dim3(256), s, ev, a); break;
+        case EPI_QKV: launch_timed(gemm_big_kernel<T, EPI_QKV>, grid, dim3(256), s, ev, a); break;
+        case EPI_SWIGLU: launch_timed(gemm_big_kernel<T, EPI_SWIGLU>, grid, dim3(256), s, ev, a); break;
+        default: break;  // the heads run on at most 64 rows (launch_gemm rejects more)
+    }
+}
+
 // Launch shape of a weight matrix, a function of (N, K) only, never of M: RT 16-row tiles
 // per workgroup (activations reused across them) and the K split over the workgroup's waves.
 // Since neither depends on M, every output's summation order is the same for every call on
@@ -239,12 +326,21 @@ static void gemm_dispatch(Epi e, const GemmArgs &a, GemmShape sh, hipStream_t s,
     }
 }
 
-void launch_gemm(DType t, Epi e, const GemmArgs &a, hipStream_t s, const LaunchEvents &ev) {
+bool launch_gemm(DType t, Epi e, const GemmArgs &a, hipStream_t s, const LaunchEvents &ev) {
+    if (a.M > 64 || a.large_m) {
+        if (e == EPI_LOGITS) return false;
+        if (t == DType::BF16)
+            launch_gemm_big<DType::BF16>(e, a, s, ev);
+        else
+            launch_gemm_big<DType::F32>(e, a, s, ev);
+        return true;
+    }
     const GemmShape sh = gemm_shape(a.N, a.K, pack_kc(t), a.M);
     if (t == DType::BF16)
         gemm_dispatch<DType::BF16>(e, a, sh, s, ev);
     else
         gemm_dispatch<DType::F32>(e, a, sh, s, ev);
+    return true;
 }
 
 // ------------------------------------------------------------------------------------------
@@ -552,6 +648,8 @@ __global__ void __launch_bounds__(64 * WPB) attn_kernel(AttnArgs a) {
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) vf[dt][ks] = mask_keys<T>(vf[dt][ks], ks * KC + EPL * lg, nk);
         for (int r0 = 0; r0 < R; r0 += 16) {
+            // a tile whose last row sits before this chunk has no keys here (prefill blocks)
+            if (len0 + min(R - 1, r0 + 15) / G < kbase) continue;  // uniform across the wave
             if (r0 > 0) load_q(r0);
             uint4 qf[DS];
             {
@@ -678,11 +776,12 @@ template <DType T, int HD>
 static void launch_attention_t(const AttnArgs &a, hipStream_t s, const LaunchEvents &ev) {
     // One wave per 64-key chunk, four chunks per workgroup: the workgroup that finishes last
     // merges with four waves.  A single query row per kv head over a small grid takes one wave
-    // per workgroup instead, which spreads the chunks over more compute units.  A large grid
-    // merges in a second launch instead: otherwise every workgroup would wait for its partial
-    // stores before counting itself done, and the last merges would run at the kernel's tail.
+    // per workgroup instead, which spreads the chunks over more compute units.  A large grid, or
+    // many query rows per kv head (prefill blocks), merges in a second launch instead: otherwise
+    // every workgroup would wait for its partial stores before counting itself done, and the
+    // last merges would run at the kernel's tail, a few waves each merging many rows.
     const long waves = (long)a.n_chunks * a.n_kv * a.B;
-    if (waves >= kAttnPackWaves) {
+    if (waves >= kAttnPackWaves || a.c * (a.n_heads / a.n_kv) > 32) {
         const int rows = a.B * a.c * a.n_heads;
         LaunchEvents e1 = ev, e2 = ev;  // one interval around both launches
         e1.stop = nullptr;
