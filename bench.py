@@ -178,7 +178,13 @@ def main():
     t = time.time()
     eng.prefill(prompts)
     torch.cuda.synchronize()
-    log("prefill %.2f s" % (time.time() - t))
+    pf_s = time.time() - t
+    # dense work of the prefill: every layer's matrices on every prompt token (+ the head on the
+    # last token of each sequence); attention adds about 2 * P * d * L per token on top
+    pf_flop = 2.0 * B * P * shape.layer_params() * shape.n_layers + 2.0 * B * shape.vocab * shape.d_model
+    prefill = {"s": round(pf_s, 4), "tokens": B * P, "gemm_tflop": round(pf_flop / 1e12, 2),
+               "tflop_s": round(pf_flop / pf_s / 1e12, 1)}
+    log("prefill %.2f s (%.1f TFLOP of GEMM work, %.0f TFLOP/s)" % (pf_s, pf_flop / 1e12, pf_flop / pf_s / 1e12))
     eng_lens = [P] * B
     for _ in range(W):
         step(k)
@@ -333,6 +339,7 @@ def main():
                        "rate": round(float(mv.mean()) / k, 4)},
         "ar_baseline": ar,
         "full_acceptance": ceil,
+        "prefill": prefill,
         "drafter_update": upd,
         "paper_context": PAPER_CONTEXT,
     }
