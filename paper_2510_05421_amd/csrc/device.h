@@ -145,11 +145,6 @@ constexpr int kCoherent = 16;  // sc1
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t coherent_rsrc(const void *base) {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, 0x7fffffff, 0x00020000);
 }
-__device__ __forceinline__ uint4 ld_coherent16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
-    typedef unsigned v4u __attribute__((ext_vector_type(4)));
-    const v4u v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kCoherent);
-    return uint4{v.x, v.y, v.z, v.w};
-}
 __device__ __forceinline__ float ld_coherent_f32(__amdgpu_buffer_rsrc_t r, uint32_t off) {
     return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kCoherent));
 }

@@ -575,7 +575,7 @@ __device__ __forceinline__ void merge_row(const AttnArgs &a, int m, int h, int n
         St<T>::store(a.O, fm_index<T>(m, h * HD + (HD / 64) * lane + q, a.n_heads * HD), o[q] / L);
 }
 
-constexpr long kAttnPackWaves = 2048;
+constexpr long kAttnLargeGrid = 2048;  // chunk-waves from which the merge takes its own launch
 
 template <DType T, int HD, int WPB, bool MERGE>
 __global__ void __launch_bounds__(64 * WPB) attn_kernel(AttnArgs a) {
@@ -781,7 +781,7 @@ static void launch_attention_t(const AttnArgs &a, hipStream_t s, const LaunchEve
     // every workgroup would wait for its partial stores before counting itself done, and the
     // last merges would run at the kernel's tail, a few waves each merging many rows.
     const long waves = (long)a.n_chunks * a.n_kv * a.B;
-    if (waves >= kAttnPackWaves || a.c * (a.n_heads / a.n_kv) > 32) {
+    if (waves >= kAttnLargeGrid || a.c * (a.n_heads / a.n_kv) > 32) {
         const int rows = a.B * a.c * a.n_heads;
         LaunchEvents e1 = ev, e2 = ev;  // one interval around both launches
         e1.stop = nullptr;
