@@ -493,23 +493,8 @@ void launch_lora_u(DType t, const void *x, const float *Bm, int M, int d, int r,
 }
 
 // ------------------------------------------------------------------------------------------
-// Block-causal attention against the KV cache, on MFMA.
-//
-// Keys are cut into 64-position chunks at absolute positions; wave w of workgroup x owns chunk
-// 4x + w of one (kv head, sequence).  The query rows that read this kv head (c tokens x
-// n_heads/n_kv grouped heads) are taken 16 at a time as the MFMA row dimension:
-//   S = Q K^T      A = query fragments, B = key fragments read straight from the key cache;
-//   softmax        per row over the chunk's 64 keys: max, p = exp(s - max), sum (fixed tree);
-//   O = P V        P goes through a per-wave LDS tile into A-operand layout; B = value
-//                  fragments read straight from the chunk-major value cache (one chunk's
-//                  [hd][64] block is contiguous, positions innermost).
-// Row at position p sees keys 0..p (block-causal); keys past a row's position, or past the
-// cached length, are masked before the max and multiply as zeros.  Each chunk's (max, sum,
-// unnormalised output) is published with agent-scope relaxed atomic stores; a per-(sequence,
-// kv head) counter then tells the workgroup that finishes last, and that one merges every row's
-// chunks in chunk order, reading them back with coherent (sc1) loads: no cache writeback, and
-// the loads stay in flight together.  Rows are independent MFMA rows and the chunk arithmetic
-// depends only on positions, so a row's result is the same whichever other rows share its block.
+// Block-causal attention against the KV cache, on MFMA: split over 64-key chunks at absolute
+// positions (attn_chunk), then a merge of every row's chunks in chunk order (merge_fold).
 // ------------------------------------------------------------------------------------------
 // One group of up to 64 chunks of a row's merge (lane = chunk for the statistics; lane holds
 // head dims PER*lane .. PER*lane + PER-1 of the outputs): the group's maximum and the rescaled sums come from wave reductions with
@@ -517,6 +502,30 @@ void launch_lora_u(DType t, const void *x, const float *Bm, int M, int d, int r,
 // unconditional (addresses clamped to the group's last chunk, weights of clamped lanes zero, so
 // they add zeros) and issued before the arithmetic that needs them: one round trip per group.
 // NB only sets how many loads are in flight; the sum is the same for every NB >= cn.
+// The arithmetic of one group, on values already loaded: my_m, my_l of chunk `lane` and the
+// output partials ov[u] of chunk u for the lane's head dims.  Every merge path runs this code,
+// so they give the same bits.
+template <int HD, int NB>
+__device__ __forceinline__ void merge_fold(float my_m, float my_l, const float (&ov)[NB][HD / 64], int cn, int lane,
+                                           float &Mr, float &L, float (&o)[HD / 64]) {
+    constexpr int PER = HD / 64;
+    const float gm = wave_max(lane < cn ? my_m : -INFINITY);
+    const float Mn = fmaxf(Mr, gm);
+    const float rs = expf(Mr - Mn);  // 0 on the first group
+    const float scl = lane < cn ? expf(my_m - Mn) : 0.f;
+    L = L * rs + wave_sum(my_l * scl);
+#pragma unroll
+    for (int q = 0; q < PER; ++q) o[q] *= rs;
+    Mr = Mn;
+#pragma unroll
+    for (int u = 0; u < NB; ++u) {
+        const float sc = __shfl(scl, u);  // zero for chunks past cn
+#pragma unroll
+        for (int q = 0; q < PER; ++q) o[q] += ov[u][q] * sc;
+    }
+}
+
+// One group from the partials in memory (coherent loads, all in flight together).
 template <int HD, int NB>
 __device__ __forceinline__ void merge_group(__amdgpu_buffer_rsrc_t mlr, __amdgpu_buffer_rsrc_t por, size_t slot,
                                             int cn, int lane, float &Mr, float &L, float (&o)[HD / 64]) {
@@ -535,20 +544,16 @@ __device__ __forceinline__ void merge_group(__amdgpu_buffer_rsrc_t mlr, __amdgpu
             ov[u][0] = ld_coherent_f32(por, off);
         }
     }
-    const float gm = wave_max(lane < cn ? my_m : -INFINITY);
-    const float Mn = fmaxf(Mr, gm);
-    const float rs = expf(Mr - Mn);  // 0 on the first group
-    const float scl = lane < cn ? expf(my_m - Mn) : 0.f;
-    L = L * rs + wave_sum(my_l * scl);
+    merge_fold<HD, NB>(my_m, my_l, ov, cn, lane, Mr, L, o);
+}
+
+// Output of one merged row: lane holds head dims PER*lane .. +PER-1.
+template <DType T, int HD>
+__device__ __forceinline__ void store_row(const AttnArgs &a, int m, int h, int lane, const float (&o)[HD / 64],
+                                          float L) {
 #pragma unroll
-    for (int q = 0; q < PER; ++q) o[q] *= rs;
-    Mr = Mn;
-#pragma unroll
-    for (int u = 0; u < NB; ++u) {
-        const float sc = __shfl(scl, u);  // zero for chunks past cn
-#pragma unroll
-        for (int q = 0; q < PER; ++q) o[q] += ov[u][q] * sc;
-    }
+    for (int q = 0; q < HD / 64; ++q)
+        St<T>::store(a.O, fm_index<T>(m, h * HD + (HD / 64) * lane + q, a.n_heads * HD), o[q] / L);
 }
 
 // Merge of one query row m of head h over its ncr chunks (one wave), then the row's output.
@@ -570,174 +575,197 @@ __device__ __forceinline__ void merge_row(const AttnArgs &a, int m, int h, int n
         else
             merge_group<HD, 64>(mlr, por, slot0 + c0, cn, lane, Mr, L, o);
     }
-#pragma unroll
-    for (int q = 0; q < HD / 64; ++q)
-        St<T>::store(a.O, fm_index<T>(m, h * HD + (HD / 64) * lane + q, a.n_heads * HD), o[q] / L);
+    store_row<T, HD>(a, m, h, lane, o, L);
 }
 
 constexpr long kAttnLargeGrid = 2048;  // chunk-waves from which the merge takes its own launch
 
-template <DType T, int HD, int WPB, bool MERGE>
-__global__ void __launch_bounds__(64 * WPB) attn_kernel(AttnArgs a) {
+// One wave's 64-key chunk ch of (sequence b, kv head kvh), nk of its keys in the cache.
+// Keys are cut into 64-position chunks at absolute positions; the query rows that read this kv
+// head (c tokens x n_heads/n_kv grouped heads) are taken 16 at a time as the MFMA row dimension:
+//   S = Q K^T      A = query fragments, B = key fragments read straight from the key cache;
+//   softmax        per row over the chunk's 64 keys: max, p = exp(s - max), sum (fixed tree);
+//   O = P V        P goes through the wave's LDS tile Ps into A-operand layout; B = value
+//                  fragments read straight from the chunk-major value cache.
+// Row at position p sees keys 0..p (block-causal); keys past a row's position, or past the
+// cached length, are masked before the max and multiply as zeros.  Each row's unnormalised
+// output, max and sum go to sink(row, head dim, value, with_stats, max, sum).  Rows are
+// independent MFMA rows and the chunk arithmetic depends only on positions, so a row's result
+// is the same whichever other rows share its block.
+template <DType T, int HD, typename Sink>
+__device__ __forceinline__ void attn_chunk(const AttnArgs &a, int b, int kvh, int ch, int len0, int nk,
+                                           typename St<T>::type (*Ps)[CK + 16 / (int)sizeof(typename St<T>::type)],
+                                           Sink &&sink) {
     typedef typename St<T>::type E;
     constexpr int KC = (T == DType::BF16) ? 32 : 16;   // reduction depth of one fragment step
     constexpr int EPL = KC / 4;                          // elements per lane per step
     constexpr int DS = HD / KC;                          // head-dim steps of S = Q K^T
     constexpr int KS = CK / KC;                          // key steps of O = P V
     constexpr int DT = HD / 16;                          // 16-wide head-dim tiles of O
+    const int lane = threadIdx.x & 63, l16 = lane & 15, lg = lane >> 4;
+    const int kbase = ch * CK;
+    const int G = a.n_heads / a.n_kv;
+    const int R = a.c * G;
+    const size_t kc0 = ((size_t)b * a.n_kv + kvh) * a.s_max + kbase;          // key rows
+    const size_t vt0 = ((size_t)b * a.n_kv + kvh) * HD * a.s_max + (size_t)ch * HD * CK;  // value chunk
+    // Query fragments of one 16-row tile: row r0 + l16, head dims step*KC + EPL*lg .. +EPL.
+    // Rows past R read row R-1 and are zeroed when packed.
+    float4 qraw[DS][EPL / 4];
+    auto load_q = [&](int r0) {
+        const int rr = min(r0 + l16, R - 1);
+        const int i = rr / G, gi = rr - i * G;
+        const float4 *qrow =
+            (const float4 *)(a.Q + ((size_t)(b * a.c + i) * a.n_heads + kvh * G + gi) * HD + EPL * lg);
+#pragma unroll
+        for (int st = 0; st < DS; ++st)
+#pragma unroll
+            for (int e4 = 0; e4 < EPL / 4; ++e4) qraw[st][e4] = qrow[(st * KC) / 4 + e4];
+    };
+    load_q(0);  // in flight together with the key and value fragments
+    // Every position of a 64-key chunk lies inside the cache row (the row length is a multiple
+    // of 64), so the fragment loads are unconditional.  Keys at or past nk (not yet written, or
+    // past the block) get score -inf below, whatever they hold, so key fragments need no mask.
+    // key fragments: tile t holds keys 16t + l16; head dims step*KC + EPL*lg .. +EPL
+    uint4 kf[4][DS];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+        const uint4 *src = (const uint4 *)((const E *)a.Kc + (kc0 + 16 * t + l16) * HD + EPL * lg);
+#pragma unroll
+        for (int st = 0; st < DS; ++st) kf[t][st] = src[st * (KC * sizeof(E) / 16)];
+    }
+    // value fragments: tile dt holds head dim 16 dt + l16; keys step*KC + EPL*lg .. +EPL.  Their
+    // probabilities are zero, but 0 * (NaN or inf) is not, so those keys are zeroed.
+    uint4 vf[DT][KS];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+        const E *src = (const E *)a.Vc + vt0 + (16 * dt + l16) * CK + EPL * lg;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) vf[dt][ks] = *(const uint4 *)(src + ks * KC);
+    }
+    // keep every load above in flight before the first use of any of them
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) vf[dt][ks] = mask_keys<T>(vf[dt][ks], ks * KC + EPL * lg, nk);
+    for (int r0 = 0; r0 < R; r0 += 16) {
+        // a tile whose last row sits before this chunk has no keys here (prefill blocks)
+        if (len0 + min(R - 1, r0 + 15) / G < kbase) continue;  // uniform across the wave
+        if (r0 > 0) load_q(r0);
+        uint4 qf[DS];
+        {
+            const bool ok = r0 + l16 < R;
+#pragma unroll
+            for (int st = 0; st < DS; ++st) {
+                float v[EPL];
+#pragma unroll
+                for (int e4 = 0; e4 < EPL / 4; ++e4) {
+                    const float4 q4 = qraw[st][e4];
+                    v[4 * e4 + 0] = ok ? q4.x : 0.f;
+                    v[4 * e4 + 1] = ok ? q4.y : 0.f;
+                    v[4 * e4 + 2] = ok ? q4.z : 0.f;
+                    v[4 * e4 + 3] = ok ? q4.w : 0.f;
+                }
+                qf[st] = pack_frag<T>(v);
+            }
+        }
+        // S: lane holds rows r0 + 4 lg + j, key 16 t + l16
+        f32x4 S[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            S[t] = (f32x4){0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int st = 0; st < DS; ++st) S[t] = St<T>::mma(qf[st], kf[t][st], S[t]);
+        }
+        float rmax[4], rsum[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int r = r0 + 4 * lg + j;
+            const int i = r / G;
+            const int nvalid = r < R ? min(nk, len0 + i + 1 - kbase) : 0;
+            float mx = -INFINITY;
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                const float sv = (16 * t + l16 < nvalid) ? S[t][j] * a.scale : -INFINITY;
+                S[t][j] = sv;
+                mx = fmaxf(mx, sv);
+            }
+#pragma unroll
+            for (int o = 1; o < 16; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+            float ps = 0.f;
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                const float pv = (mx == -INFINITY) ? 0.f : expf(S[t][j] - mx);
+                S[t][j] = pv;
+                ps += pv;
+            }
+#pragma unroll
+            for (int o = 1; o < 16; o <<= 1) ps += __shfl_xor(ps, o);
+            rmax[j] = mx;
+            rsum[j] = ps;
+        }
+        // P -> LDS (row-major, dtype), then read back as A fragments
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) St<T>::store(&Ps[4 * lg + j][0], 16 * t + l16, S[t][j]);
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        uint4 pf[KS];
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) pf[ks] = *(const uint4 *)&Ps[l16][ks * KC + EPL * lg];
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        // O: lane holds rows r0 + 4 lg + j, head dim 16 dt + l16
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+            f32x4 O = (f32x4){0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) O = St<T>::mma(pf[ks], vf[dt][ks], O);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int r = r0 + 4 * lg + j;
+                if (r < R && rmax[j] != -INFINITY) sink(r, 16 * dt + l16, O[j], dt == 0 && l16 == 0, rmax[j], rsum[j]);
+            }
+        }
+    }
+}
+
+// Split-KV decode attention on MFMA: wave w of workgroup x owns chunk WPB x + w of one
+// (sequence, kv head).  Each chunk's (max, sum, unnormalised output) is published with
+// agent-scope relaxed stores.  With MERGE, a per-(sequence, kv head) counter then tells the
+// workgroup that finishes last, and that one merges every row's chunks in chunk order, reading
+// them back with coherent (sc1) loads: no cache writeback, and the loads stay in flight together.
+template <DType T, int HD, int WPB, bool MERGE>
+__global__ void __launch_bounds__(64 * WPB) attn_kernel(AttnArgs a) {
+    typedef typename St<T>::type E;
     constexpr int PST = CK + 16 / (int)sizeof(E);        // padded LDS row of P (elements)
     __shared__ __align__(16) E Ps[WPB][16][PST];
     __shared__ int is_last;
 
     const int kvh = blockIdx.y, b = blockIdx.z;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const int l16 = lane & 15, lg = lane >> 4;
     const int len0 = a.lens[b] + a.pos_off;
     const int pmax = len0 + a.c - 1;
     const int nch = pmax / CK + 1;
     if (WPB * (int)blockIdx.x >= nch) return;  // uniform across the workgroup
     const int ch = WPB * blockIdx.x + w;
-    const bool active = ch < nch;             // uniform across the wave
-    const int kbase = ch * CK;
-    const int nk = active ? min(CK, pmax + 1 - kbase) : 0;
     const int G = a.n_heads / a.n_kv;
     const int R = a.c * G;
-    const size_t kc0 = ((size_t)b * a.n_kv + kvh) * a.s_max + kbase;          // key rows
-    const size_t vt0 = ((size_t)b * a.n_kv + kvh) * HD * a.s_max + (size_t)ch * HD * CK;  // value chunk
-    const uint4 zero = {0u, 0u, 0u, 0u};
-
-    if (active) {
-        // Query fragments of one 16-row tile: row r0 + l16, head dims step*KC + EPL*lg .. +EPL.
-        // Rows past R read row R-1 and are zeroed when packed.
-        float4 qraw[DS][EPL / 4];
-        auto load_q = [&](int r0) {
-            const int rr = min(r0 + l16, R - 1);
-            const int i = rr / G, gi = rr - i * G;
-            const float4 *qrow =
-                (const float4 *)(a.Q + ((size_t)(b * a.c + i) * a.n_heads + kvh * G + gi) * HD + EPL * lg);
-#pragma unroll
-            for (int st = 0; st < DS; ++st)
-#pragma unroll
-                for (int e4 = 0; e4 < EPL / 4; ++e4) qraw[st][e4] = qrow[(st * KC) / 4 + e4];
-        };
-        load_q(0);  // in flight together with the key and value fragments
-        // Every position of a 64-key chunk lies inside the cache row (the row length is a multiple
-        // of 64), so the fragment loads are unconditional.  Keys at or past nk (not yet written, or
-        // past the block) get score -inf below, whatever they hold, so key fragments need no mask.
-        // key fragments: tile t holds keys 16t + l16; head dims step*KC + EPL*lg .. +EPL
-        uint4 kf[4][DS];
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-            const uint4 *src = (const uint4 *)((const E *)a.Kc + (kc0 + 16 * t + l16) * HD + EPL * lg);
-#pragma unroll
-            for (int st = 0; st < DS; ++st) kf[t][st] = src[st * (KC * sizeof(E) / 16)];
-        }
-        // value fragments: tile dt holds head dim 16 dt + l16; keys step*KC + EPL*lg .. +EPL.  Their
-        // probabilities are zero, but 0 * (NaN or inf) is not, so those keys are zeroed.
-        uint4 vf[DT][KS];
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) {
-            const E *src = (const E *)a.Vc + vt0 + (16 * dt + l16) * CK + EPL * lg;
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks) vf[dt][ks] = *(const uint4 *)(src + ks * KC);
-        }
-        // keep every load above in flight before the first use of any of them
-        __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks) vf[dt][ks] = mask_keys<T>(vf[dt][ks], ks * KC + EPL * lg, nk);
-        for (int r0 = 0; r0 < R; r0 += 16) {
-            // a tile whose last row sits before this chunk has no keys here (prefill blocks)
-            if (len0 + min(R - 1, r0 + 15) / G < kbase) continue;  // uniform across the wave
-            if (r0 > 0) load_q(r0);
-            uint4 qf[DS];
-            {
-                const bool ok = r0 + l16 < R;
-#pragma unroll
-                for (int st = 0; st < DS; ++st) {
-                    float v[EPL];
-#pragma unroll
-                    for (int e4 = 0; e4 < EPL / 4; ++e4) {
-                        const float4 q4 = qraw[st][e4];
-                        v[4 * e4 + 0] = ok ? q4.x : 0.f;
-                        v[4 * e4 + 1] = ok ? q4.y : 0.f;
-                        v[4 * e4 + 2] = ok ? q4.z : 0.f;
-                        v[4 * e4 + 3] = ok ? q4.w : 0.f;
-                    }
-                    qf[st] = pack_frag<T>(v);
-                }
-            }
-            // S: lane holds rows r0 + 4 lg + j, key 16 t + l16
-            f32x4 S[4];
-#pragma unroll
-            for (int t = 0; t < 4; ++t) {
-                S[t] = (f32x4){0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int st = 0; st < DS; ++st) S[t] = St<T>::mma(qf[st], kf[t][st], S[t]);
-            }
-            float rmax[4], rsum[4];
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int r = r0 + 4 * lg + j;
-                const int i = r / G;
-                const int nvalid = r < R ? min(nk, len0 + i + 1 - kbase) : 0;
-                float mx = -INFINITY;
-#pragma unroll
-                for (int t = 0; t < 4; ++t) {
-                    const float sv = (16 * t + l16 < nvalid) ? S[t][j] * a.scale : -INFINITY;
-                    S[t][j] = sv;
-                    mx = fmaxf(mx, sv);
-                }
-#pragma unroll
-                for (int o = 1; o < 16; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
-                float ps = 0.f;
-#pragma unroll
-                for (int t = 0; t < 4; ++t) {
-                    const float pv = (mx == -INFINITY) ? 0.f : expf(S[t][j] - mx);
-                    S[t][j] = pv;
-                    ps += pv;
-                }
-#pragma unroll
-                for (int o = 1; o < 16; o <<= 1) ps += __shfl_xor(ps, o);
-                rmax[j] = mx;
-                rsum[j] = ps;
-            }
-            // P -> LDS (row-major, dtype), then read back as A fragments
-#pragma unroll
-            for (int t = 0; t < 4; ++t)
-#pragma unroll
-                for (int j = 0; j < 4; ++j) St<T>::store(&Ps[w][4 * lg + j][0], 16 * t + l16, S[t][j]);
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-            __builtin_amdgcn_wave_barrier();
-            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-            uint4 pf[KS];
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks) pf[ks] = *(const uint4 *)&Ps[w][l16][ks * KC + EPL * lg];
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-            __builtin_amdgcn_wave_barrier();
-            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-            // O: lane holds rows r0 + 4 lg + j, head dim 16 dt + l16
-#pragma unroll
-            for (int dt = 0; dt < DT; ++dt) {
-                f32x4 O = (f32x4){0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int ks = 0; ks < KS; ++ks) O = St<T>::mma(pf[ks], vf[dt][ks], O);
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const int r = r0 + 4 * lg + j;
-                    if (r < R && rmax[j] != -INFINITY) {
-                        const int i = r / G, gi = r - i * G;
-                        const size_t slot = ((size_t)(b * a.c + i) * a.n_heads + kvh * G + gi) * a.chunk_stride + ch;
-                        st_agent(a.part_o + slot * HD + 16 * dt + l16, O[j]);
-                        if (dt == 0 && l16 == 0) {
-                            st_agent(a.part_ml + slot * 2 + 0, rmax[j]);
-                            st_agent(a.part_ml + slot * 2 + 1, rsum[j]);
-                        }
-                    }
-                }
-            }
-        }
+    if (ch < nch) {  // uniform across the wave
+        attn_chunk<T, HD>(a, b, kvh, ch, len0, min(CK, pmax + 1 - ch * CK), Ps[w],
+                          [&](int r, int dim, float v, bool stats, float mx, float sm) {
+                              const int i = r / G, gi = r - i * G;
+                              const size_t slot =
+                                  ((size_t)(b * a.c + i) * a.n_heads + kvh * G + gi) * a.chunk_stride + ch;
+                              st_agent(a.part_o + slot * HD + dim, v);
+                              if (stats) {
+                                  st_agent(a.part_ml + slot * 2 + 0, mx);
+                                  st_agent(a.part_ml + slot * 2 + 1, sm);
+                              }
+                          });
     }
 
     // Without MERGE, attn_merge_kernel merges in a launch of its own and this workgroup is done.
@@ -781,13 +809,14 @@ static void launch_attention_t(const AttnArgs &a, hipStream_t s, const LaunchEve
     // every workgroup would wait for its partial stores before counting itself done, and the
     // last merges would run at the kernel's tail, a few waves each merging many rows.
     const long waves = (long)a.n_chunks * a.n_kv * a.B;
-    if (waves >= kAttnLargeGrid || a.c * (a.n_heads / a.n_kv) > 32) {
-        const int rows = a.B * a.c * a.n_heads;
+    const int rows = a.c * (a.n_heads / a.n_kv);
+    if (waves >= kAttnLargeGrid || rows > 32) {
+        const int all_rows = a.B * a.c * a.n_heads;
         LaunchEvents e1 = ev, e2 = ev;  // one interval around both launches
         e1.stop = nullptr;
         e2.start = nullptr;
         launch_timed(attn_kernel<T, HD, 4, false>, dim3((a.n_chunks + 3) / 4, a.n_kv, a.B), dim3(256), s, e1, a);
-        launch_timed(attn_merge_kernel<T, HD>, dim3((rows + 3) / 4), dim3(256), s, e2, a);
+        launch_timed(attn_merge_kernel<T, HD>, dim3((all_rows + 3) / 4), dim3(256), s, e2, a);
     } else if (a.c * (a.n_heads / a.n_kv) == 1) {
         launch_timed(attn_kernel<T, HD, 1, true>, dim3(a.n_chunks, a.n_kv, a.B), dim3(64), s, ev, a);
     } else {
