@@ -421,3 +421,30 @@ def test_sampled_drafting_is_lossless_and_changes_drafts():
     _say("sampled drafting: mean m %.2f vs argmax drafting %.2f" % (samp_info["m"].mean(), greedy_info["m"].mean()))
     assert samp_info["steps"] != greedy_info["steps"] or not np.array_equal(samp_info["m"], greedy_info["m"])
     eng.close()
+
+
+@pytest.mark.parametrize("B,P,k", [(4, 1, 16), (1, 1, 16), (64, 8, 1), (16, 3, 4)])
+def test_edge_shapes_are_lossless(B, P, k):
+    """Degenerate and maximum shapes: one-token prompts, the largest k_spec (16), the widest
+    block (4 x 16 = 64 rows) and the widest batch (64 sequences): speculative decoding equals
+    greedy decoding bitwise, up to the last position of the cache, and sequence 0 agrees with
+    the oracle."""
+    shape = gu.SHAPES["tiny"]
+    T = 40
+    prompts = synth.make_prompts(shape.vocab, B, P, 13)
+    w = synth.make_weights(shape, 0, lora_A_std=0.05)
+    max_seq = P + T + k          # a step may write k_spec positions past the last committed token
+    eng, _ = gu.engine(shape, max_batch=B, max_seq=max_seq, max_k_spec=k, weights=w)
+    spec, info = eng.generate(prompts, T, k)
+    lens = eng.lengths().copy()
+    kv = [eng.read_kv(l, b, 0, int(lens[b])) for l in (0, shape.n_layers - 1) for b in (0, B - 1)]
+    ar, _ = eng.generate(prompts, T, 1)
+    assert np.array_equal(spec, ar)
+    kv_ar = [eng.read_kv(l, b, 0, int(lens[b])) for l in (0, shape.n_layers - 1) for b in (0, B - 1)]
+    for (k1, v1), (k2, v2) in zip(kv, kv_ar):
+        assert np.array_equal(k1, k2) and np.array_equal(v1, v2)
+    ref = odvi.greedy_ar(oracle.OracleModel(w), prompts[0], T)
+    agree = gu.compare_free_running(spec[0], ref.tokens, ref.gaps)
+    _say("edge B=%d P=%d k_spec=%d: %d steps, mean m %.2f, %d/%d tokens agree with the oracle"
+         % (B, P, k, info["steps"], info["m"].mean(), agree, T))
+    eng.close()
