@@ -328,6 +328,31 @@ def test_state_capacity_and_numeric_errors():
     eng.close()
 
 
+def test_sampling_and_graph_settings_are_checked():
+    """dvi_set_sampling rejects negative or non-finite temperatures and changes during a step;
+    neither setting leaves the context unusable."""
+    from paper_2510_05421_amd._abi import DVIError, ERR_STATE, ERR_ARG
+    shape = gu.SHAPES["tiny"]
+    eng, _ = gu.engine(shape, max_seq=64)
+    for bad in (-1.0, float("nan"), float("inf")):
+        with pytest.raises(DVIError) as e:
+            eng.set_sampling(bad, 1)
+        assert e.value.status == ERR_ARG
+    eng.prefill(synth.make_prompts(shape.vocab, 1, 8, 0))
+    eng.draft(2)
+    with pytest.raises(DVIError) as e:
+        eng.set_sampling(1.0, 1)
+    assert e.value.status == ERR_STATE
+    eng.verify()
+    eng.commit()
+    eng.set_sampling(0.5, 2)
+    eng.set_graphs(False)
+    eng.set_graphs(True)
+    toks, info = eng.generate(synth.make_prompts(shape.vocab, 1, 8, 0), 12, 4)
+    assert toks.shape == (1, 12)
+    eng.close()
+
+
 @pytest.mark.parametrize("tau", [0.0, 1.0])
 def test_graph_replay_equals_direct_launches(tau):
     """Draft and verify replayed from captured HIP graphs give the tokens, accept lengths, keys,
