@@ -127,7 +127,7 @@ dvi_status dvi_create(const dvi_config *cfg, const dvi_weights *w, void *workspa
 void dvi_destroy(dvi_ctx *ctx);
 
 /*
- * Prefill (Section 3.3, "compute the shallow state once given the prefix"):
+ * Prefill (Section 3.3: the shallow state is computed once from the prefix):
  * run all L layers over each sequence's prompt, fill the KV cache, and emit
  * each sequence's first token x_P = argmax p_phi(. | h_{L,P-1}).  ids: HOST
  * int32 [batch, stride]; lens: HOST int32 [batch], all equal in this version,

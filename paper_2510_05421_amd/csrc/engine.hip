@@ -20,7 +20,7 @@ using namespace dvi;
 
 namespace {
 
-constexpr int kMaxRows = 64;   // tokens per GEMM call (four 16-wide MFMA groups)
+constexpr int kMaxRows = 64;   // rows of a decode-step GEMM (four 16-wide MFMA groups)
 
 enum State { S_CREATED = 0, S_READY, S_DRAFTED, S_VERIFIED };
 
