@@ -101,39 +101,34 @@ __global__ void __launch_bounds__(64 * WMAX) gemm_kernel(GemmArgs a) {
     EpiOperands<MG> pre;
     if (kEarly && wave < RT) epilogue_prefetch<MG, EPI>(a, nt0 + wave, pre);
 
-    // Each activation fragment feeds RT weight tiles.  The loop is software-pipelined: the
-    // fragments of the next U chunks are requested before the current U are multiplied, so a
-    // wave always has loads in flight while its MFMAs run.
-    constexpr int U = 2;
-    const uint4 zero = {0u, 0u, 0u, 0u};
-    uint4 w[U][RT], x[U][MG];
-    auto fetch = [&](int cb, uint4 (&wf)[U][RT], uint4 (&xf)[U][MG]) {
+    // Each activation fragment feeds RT weight tiles.  Loads go through a ring of S stages,
+    // stage st holding chunk c + st: once a stage's MFMAs have issued it is refilled with the
+    // chunk S ahead, so S - 1 chunks are always in flight while one is multiplied (the same
+    // registers as double-buffering S/2 chunks, with more of them in flight).  Chunks are
+    // accumulated in order c0, c0 + 1, ..., c1 - 1 whatever S is.
+    constexpr int S = 4;
+    uint4 w[S][RT], x[S][MG];
+    auto fetch = [&](int cb, uint4 (&wf)[RT], uint4 (&xf)[MG]) {
+        const bool in = cb < c1;
+        const uint4 zero = {0u, 0u, 0u, 0u};
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const bool in = cb + u < c1;
+        for (int t = 0; t < RT; ++t) wf[t] = in ? ld_stream(wp + t * tile_stride + (size_t)cb * 64) : zero;
 #pragma unroll
-            for (int t = 0; t < RT; ++t) wf[u][t] = in ? ld_stream(wp + t * tile_stride + (size_t)(cb + u) * 64) : zero;
-#pragma unroll
-            for (int g = 0; g < MG; ++g) xf[u][g] = (in && xv[g]) ? ld_stream(xp[g] + (size_t)(cb + u) * 64) : zero;
-        }
+        for (int g = 0; g < MG; ++g) xf[g] = (in && xv[g]) ? ld_stream(xp[g] + (size_t)cb * 64) : zero;
     };
-    fetch(c0, w, x);
+#pragma unroll
+    for (int st = 0; st < S; ++st) fetch(c0 + st, w[st], x[st]);
     if (kEarly && wave < RT) epilogue_prefetch_rope<MG, EPI>(a, nt0 + wave, pre);
-    for (int c = c0; c < c1; c += U) {
-        uint4 wn[U][RT], xn[U][MG];
-        fetch(c + U, wn, xn);
+    for (int c = c0; c < c1; c += S) {
 #pragma unroll
-        for (int u = 0; u < U; ++u)
+        for (int st = 0; st < S; ++st) {
+            if (c + st < c1) {  // uniform across the wave
 #pragma unroll
-            for (int t = 0; t < RT; ++t)
+                for (int t = 0; t < RT; ++t)
 #pragma unroll
-                for (int g = 0; g < MG; ++g) acc[t][g] = St<T>::mma(w[u][t], x[u][g], acc[t][g]);
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-#pragma unroll
-            for (int t = 0; t < RT; ++t) w[u][t] = wn[u][t];
-#pragma unroll
-            for (int g = 0; g < MG; ++g) x[u][g] = xn[u][g];
+                    for (int g = 0; g < MG; ++g) acc[t][g] = St<T>::mma(w[st][t], x[st][g], acc[t][g]);
+            }
+            fetch(c + S + st, w[st], x[st]);
         }
     }
 
