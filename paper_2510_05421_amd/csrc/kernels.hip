@@ -262,9 +262,10 @@ struct GemmShape {
 static GemmShape gemm_shape(int N, int K, int KC, int M) {
     const int tiles = N / 16, chunks = K / KC, mg = (M + 15) / 16;
     // K split, from the matrix only: the most waves per workgroup (up to 16) that keep the whole
-    // grid resident at once (8 waves per SIMD x 4 SIMDs x 256 CUs) with >= 4 chunks per wave.
+    // grid resident at once (8 waves per SIMD x 4 SIMDs x 256 CUs), and at least 8 (more loads in
+    // flight per tile beats residency for the widest matrices), with >= 4 chunks per wave.
     int w = 1;
-    while (w < 16 && (long)tiles * (2 * w) <= 8192 && chunks / (2 * w) >= 4) w *= 2;
+    while (w < 16 && ((long)tiles * (2 * w) <= 8192 || w < 8) && chunks / (2 * w) >= 4) w *= 2;
     // tiles per workgroup: more when there are more token groups to reuse each weight tile on
     // (16-wave workgroups have 128 registers per lane and keep one tile)
     int rt = 1;
