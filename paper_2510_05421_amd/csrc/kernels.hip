@@ -47,11 +47,11 @@ void launch_pack(DType t, PackSrc srcs, const int32_t *prow, int N, int K, void 
 // ------------------------------------------------------------------------------------------
 // Skinny-M weight-streaming GEMM:  Y[m][n] = sum_k X[m][k] W[n][k],  M <= 64.
 //
-// One workgroup owns a band of 16 output features (one packed tile row) for all M tokens.
+// One workgroup owns RT bands of 16 output features (packed tile rows) for all M tokens.
 // Its waves split the K range into contiguous pieces (split fixed by K and the wave count,
-// which depends only on N), each wave streaming 1 KiB weight fragments straight into MFMA
-// A operands; tokens are the MFMA B operand (16 per group, MG groups).  The per-wave
-// partial tiles are summed in wave order through LDS and the epilogue runs on wave 0.
+// which depends only on the matrix shape), each wave streaming 1 KiB weight fragments straight
+// into MFMA A operands; tokens are the MFMA B operand (16 per group, MG groups).  The per-wave
+// partial tiles are summed in wave order through LDS and tile t's epilogue runs on wave t.
 // Output layout of a 16x16 MFMA tile: lane l holds rows 4*(l/16)+j (j = 0..3) of column
 // l % 16, i.e. features nt*16 + 4*(l/16) + j of token 16*g + (l % 16).
 //
