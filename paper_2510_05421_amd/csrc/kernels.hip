@@ -888,55 +888,72 @@ void launch_argmax(const float *pv, const int32_t *pi, int M, int ntiles, int32_
 
 // ------------------------------------------------------------------------------------------
 // Commit: longest agreeing prefix, length advance (the rollback), pending token, replay log.
-// One thread does the whole (tiny) bookkeeping so ring slots are assigned in sequence order.
+// One wave; lane b owns sequence b (batch <= 64).  m_b is the number of leading agreements of
+// drafts and targets, read off the lane's mismatch bits.  The replay rows of every sequence get
+// consecutive ring slots in sequence order from a wave prefix sum of the per-sequence row
+// counts.  A step that logs more rows than the ring holds keeps its last ring_rows rows, the ones
+// that would survive logging the rows one by one, so no two rows share a slot.
 // ------------------------------------------------------------------------------------------
-__global__ void commit_kernel(CommitArgs a) {
-    if (threadIdx.x != 0 || blockIdx.x != 0) return;
-    const int k = a.k_spec;
-    int next = a.ring_state[0], valid = a.ring_state[1], cnt = 0;
-    if (a.flags[0] != 0) {
-        for (int b = 0; b < a.B; ++b) {
+__global__ void __launch_bounds__(64) commit_kernel(CommitArgs a) {
+    const int lane = threadIdx.x, b = lane, k = a.k_spec;
+    const bool act = b < a.B;
+    if (a.flags[0] != 0) {  // non-finite logits: nothing is committed
+        if (act) {
             for (int i = 0; i < k; ++i) a.tokens_out[(size_t)b * k + i] = -1;
             a.n_out[b] = 0;
             a.m_out[b] = 0;
         }
-        a.copy_list[0] = 0;
+        if (lane == 0) a.copy_list[0] = 0;
         return;
     }
-    for (int b = 0; b < a.B; ++b) {
-        const int32_t *dr = a.drafts + (size_t)b * k;
+    const int next = a.ring_state[0], valid = a.ring_state[1];
+    int m = 0, rows = 0, prev0 = 0;
+    const int32_t *dr = a.drafts + (size_t)b * k;
+    if (act) {
         const int32_t *tg = a.targets + (size_t)b * k;
-        int m = 0;
-        while (m < k && dr[m] == tg[m]) ++m;
+        uint32_t miss = 1u << k;  // bit i: draft i disagrees (bit k stops the count)
+        for (int i = 0; i < k; ++i) miss |= (uint32_t)(dr[i] != tg[i]) << i;
+        m = __builtin_ctz(miss);
         const int lim = a.max_new ? max(a.max_new[b], 0) : k;
         const int n = min(min(m + 1, k), lim);
-        const int prev0 = a.pending[b];
+        prev0 = a.pending[b];
         for (int i = 0; i < k; ++i) a.tokens_out[(size_t)b * k + i] = i < n ? tg[i] : -1;
         a.lens[b] += n;
         if (n > 0) a.pending[b] = tg[n - 1];
         a.n_out[b] = n;
         a.m_out[b] = m;
-        if (lim > 0 && a.ring_rows > 0) {
-            const int rows = min(m + 1, k);
-            for (int i = 1; i <= rows; ++i) {
-                const int slot = next;
-                next = (next + 1) % a.ring_rows;
-                valid = min(valid + 1, a.ring_rows);
-                a.ring_a[slot] = dr[i - 1];
-                a.ring_r[slot] = (int8_t)(i <= m ? 1 : 0);
-                a.ring_i[slot] = i;
-                a.ring_prev[slot] = i == 1 ? prev0 : dr[i - 2];
-                a.ring_fresh[slot] = 1;
-                a.copy_list[1 + 2 * cnt] = b * k + i - 1;
-                a.copy_list[2 + 2 * cnt] = slot;
-                ++cnt;
-            }
-        }
+        rows = (lim > 0 && a.ring_rows > 0) ? min(m + 1, k) : 0;
     }
-    a.copy_list[0] = cnt;
-    a.ring_state[0] = next;
-    a.ring_state[1] = valid;
-    a.rng_step[0] += 1;
+    // inclusive prefix sum of the row counts over the lanes (sequence order)
+    int incl = rows;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int t = __shfl_up(incl, o);
+        if (lane >= o) incl += t;
+    }
+    const int total = __shfl(incl, 63);
+    const int first_kept = a.ring_rows > 0 ? max(total - a.ring_rows, 0) : total;
+    for (int i = 1; i <= rows; ++i) {
+        const int g = incl - rows + i - 1;  // row index within this step, in sequence order
+        if (g < first_kept) continue;
+        const int slot = (next + g) % a.ring_rows;
+        a.ring_a[slot] = dr[i - 1];
+        a.ring_r[slot] = (int8_t)(i <= m ? 1 : 0);
+        a.ring_i[slot] = i;
+        a.ring_prev[slot] = i == 1 ? prev0 : dr[i - 2];
+        a.ring_fresh[slot] = 1;
+        const int e = g - first_kept;
+        a.copy_list[1 + 2 * e] = b * k + i - 1;
+        a.copy_list[2 + 2 * e] = slot;
+    }
+    if (lane == 0) {
+        a.copy_list[0] = total - first_kept;
+        if (a.ring_rows > 0) {
+            a.ring_state[0] = (next + total) % a.ring_rows;
+            a.ring_state[1] = min(valid + total, a.ring_rows);
+        }
+        a.rng_step[0] += 1;
+    }
 }
 
 void launch_commit(const CommitArgs &a, hipStream_t s) { commit_kernel<<<1, 64, 0, s>>>(a); }

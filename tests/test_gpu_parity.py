@@ -149,6 +149,57 @@ def test_every_accept_length_and_replay_rows(j):
     eng.close()
 
 
+def test_replay_ring_smaller_than_one_steps_rows():
+    """Four sequences with accept lengths 0..3 log 10 rows per step into a 5-row ring: the ring
+    must hold exactly what logging the rows one by one, in sequence order, leaves (Section 3.3
+    logging rule; the last writer of a slot wins), with each kept row's verify logits."""
+    shape = gu.SHAPES["tiny"]
+    B, P, T, k, R = 4, 24, 22, 4, 5
+    prompts = synth.make_prompts(shape.vocab, B, P, 11)
+    eng, _ = gu.engine(shape, max_batch=B, max_seq=P + T + 16, buffer_rows=R)
+    first = eng.prefill(prompts)
+    ar = [[int(first[b])] for b in range(B)]
+    while len(ar[0]) < T:  # each sequence's greedy continuation on the same engine
+        eng.draft(1)
+        eng.verify()
+        tok, n, m = eng.commit()
+        for b in range(B):
+            ar[b].append(int(tok[b, 0]))
+    ar = np.array(ar, np.int32)
+    first = eng.prefill(prompts)
+    out = [[int(first[b])] for b in range(B)]
+    ring, nxt, valid = [None] * R, 0, 0
+    for step in range(4):
+        forced = np.zeros((B, k), np.int32)
+        for b in range(B):
+            L = len(out[b])
+            forced[b] = ar[b, L:L + k]
+            forced[b, b] = (forced[b, b] + 1) % shape.vocab  # sequence b accepts exactly b drafts
+        eng.draft(k, forced=forced)
+        eng.verify()
+        lg = eng.read_logits()
+        tok, n, m = eng.commit()
+        assert list(m) == list(range(B)), (step, m)
+        for b in range(B):
+            for i in range(1, min(m[b] + 1, k) + 1):
+                prev = out[b][-1] if i == 1 else forced[b, i - 2]
+                ring[nxt] = (forced[b, i - 1], int(i <= m[b]), i, prev, lg[b, i - 1].copy())
+                nxt, valid = (nxt + 1) % R, min(valid + 1, R)
+            out[b].extend(int(t) for t in tok[b, :n[b]])
+        assert eng.buffer_info() == (valid, nxt)
+        buf = eng.read_buffer(0, valid)
+        for sl in range(valid):
+            a_, r_, i_, prev_, lgs = ring[sl]
+            assert (buf["a"][sl], buf["r"][sl], buf["i"][sl], buf["prev"][sl], buf["fresh"][sl]) == \
+                (a_, r_, i_, prev_, 1), (step, sl)
+            assert np.array_equal(buf["logits"][sl], lgs), (step, sl)
+        ms = (buf["h"].astype(np.float64) ** 2).mean(axis=1)  # RMSNorm(h_k) rows, unit gain
+        assert np.allclose(ms, 1.0, atol=1e-4)
+    for b in range(B):
+        assert np.array_equal(np.array(out[b]), ar[b, :len(out[b])])
+    eng.close()
+
+
 def test_buffer_rows_hold_the_verify_logits_and_normed_states():
     shape = gu.SHAPES["tiny"]
     g = gu.golden("tiny")
