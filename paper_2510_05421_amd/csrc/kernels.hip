@@ -588,26 +588,27 @@ constexpr long kAttnLargeGrid = 2048;  // chunk-waves from which the merge takes
 // output, max and sum go to sink(row, head dim, value, with_stats, max, sum).  Rows are
 // independent MFMA rows and the chunk arithmetic depends only on positions, so a row's result
 // is the same whichever other rows share its block.
-template <DType T, int HD, typename Sink>
-__device__ __forceinline__ void attn_chunk(const AttnArgs &a, int b, int kvh, int ch, int len0, int nk,
-                                           typename St<T>::type (*Ps)[CK + 16 / (int)sizeof(typename St<T>::type)],
-                                           Sink &&sink) {
+//
+// The pieces below are shared by both chunk routines (all loads first for many query tiles;
+// values after the scores for one tile), so every launch shape gives the same bits.
+template <DType T, int HD>
+struct AttnTile {
     typedef typename St<T>::type E;
-    constexpr int KC = (T == DType::BF16) ? 32 : 16;   // reduction depth of one fragment step
-    constexpr int EPL = KC / 4;                          // elements per lane per step
-    constexpr int DS = HD / KC;                          // head-dim steps of S = Q K^T
-    constexpr int KS = CK / KC;                          // key steps of O = P V
-    constexpr int DT = HD / 16;                          // 16-wide head-dim tiles of O
-    const int lane = threadIdx.x & 63, l16 = lane & 15, lg = lane >> 4;
-    const int kbase = ch * CK;
-    const int G = a.n_heads / a.n_kv;
-    const int R = a.c * G;
-    const size_t kc0 = ((size_t)b * a.n_kv + kvh) * a.s_max + kbase;          // key rows
-    const size_t vt0 = ((size_t)b * a.n_kv + kvh) * HD * a.s_max + (size_t)ch * HD * CK;  // value chunk
+    static constexpr int KC = (T == DType::BF16) ? 32 : 16;  // reduction depth of one fragment step
+    static constexpr int EPL = KC / 4;                        // elements per lane per step
+    static constexpr int DS = HD / KC;                        // head-dim steps of S = Q K^T
+    static constexpr int KS = CK / KC;                        // key steps of O = P V
+    static constexpr int DT = HD / 16;                        // 16-wide head-dim tiles of O
+    static constexpr int PST = CK + 16 / (int)sizeof(E);      // padded LDS row of P (elements)
+    typedef float4 QRaw[DS][EPL / 4];
+    typedef uint4 KFrag[4][DS];
+    typedef uint4 VFrag[DT][KS];
+
     // Query fragments of one 16-row tile: row r0 + l16, head dims step*KC + EPL*lg .. +EPL.
     // Rows past R read row R-1 and are zeroed when packed.
-    float4 qraw[DS][EPL / 4];
-    auto load_q = [&](int r0) {
+    static __device__ __forceinline__ void load_q(const AttnArgs &a, int b, int kvh, int r0, QRaw &qraw) {
+        const int lane = threadIdx.x & 63, l16 = lane & 15, lg = lane >> 4;
+        const int G = a.n_heads / a.n_kv, R = a.c * G;
         const int rr = min(r0 + l16, R - 1);
         const int i = rr / G, gi = rr - i * G;
         const float4 *qrow =
@@ -616,63 +617,66 @@ __device__ __forceinline__ void attn_chunk(const AttnArgs &a, int b, int kvh, in
         for (int st = 0; st < DS; ++st)
 #pragma unroll
             for (int e4 = 0; e4 < EPL / 4; ++e4) qraw[st][e4] = qrow[(st * KC) / 4 + e4];
-    };
-    load_q(0);  // in flight together with the key and value fragments
-    // Every position of a 64-key chunk lies inside the cache row (the row length is a multiple
-    // of 64), so the fragment loads are unconditional.  Keys at or past nk (not yet written, or
-    // past the block) get score -inf below, whatever they hold, so key fragments need no mask.
-    // key fragments: tile t holds keys 16t + l16; head dims step*KC + EPL*lg .. +EPL
-    uint4 kf[4][DS];
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-        const uint4 *src = (const uint4 *)((const E *)a.Kc + (kc0 + 16 * t + l16) * HD + EPL * lg);
-#pragma unroll
-        for (int st = 0; st < DS; ++st) kf[t][st] = src[st * (KC * sizeof(E) / 16)];
     }
-    // value fragments: tile dt holds head dim 16 dt + l16; keys step*KC + EPL*lg .. +EPL.  Their
-    // probabilities are zero, but 0 * (NaN or inf) is not, so those keys are zeroed.
-    uint4 vf[DT][KS];
+    // Every position of a 64-key chunk lies inside the cache row (the row length is a multiple of
+    // 64), so the fragment loads are unconditional.  Keys at or past nk (not yet written, or past
+    // the block) get score -inf, whatever they hold, so key fragments need no mask.
+    // Key fragments: tile t holds keys 16t + l16; head dims step*KC + EPL*lg .. +EPL.
+    static __device__ __forceinline__ void load_k(const AttnArgs &a, int b, int kvh, int ch, KFrag &kf) {
+        const int lane = threadIdx.x & 63, l16 = lane & 15, lg = lane >> 4;
+        const size_t kc0 = ((size_t)b * a.n_kv + kvh) * a.s_max + (size_t)ch * CK;
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) {
-        const E *src = (const E *)a.Vc + vt0 + (16 * dt + l16) * CK + EPL * lg;
+        for (int t = 0; t < 4; ++t) {
+            const uint4 *src = (const uint4 *)((const E *)a.Kc + (kc0 + 16 * t + l16) * HD + EPL * lg);
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) vf[dt][ks] = *(const uint4 *)(src + ks * KC);
-    }
-    // keep every load above in flight before the first use of any of them
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) vf[dt][ks] = mask_keys<T>(vf[dt][ks], ks * KC + EPL * lg, nk);
-    for (int r0 = 0; r0 < R; r0 += 16) {
-        // a tile whose last row sits before this chunk has no keys here (prefill blocks)
-        if (len0 + min(R - 1, r0 + 15) / G < kbase) continue;  // uniform across the wave
-        if (r0 > 0) load_q(r0);
-        uint4 qf[DS];
-        {
-            const bool ok = r0 + l16 < R;
-#pragma unroll
-            for (int st = 0; st < DS; ++st) {
-                float v[EPL];
-#pragma unroll
-                for (int e4 = 0; e4 < EPL / 4; ++e4) {
-                    const float4 q4 = qraw[st][e4];
-                    v[4 * e4 + 0] = ok ? q4.x : 0.f;
-                    v[4 * e4 + 1] = ok ? q4.y : 0.f;
-                    v[4 * e4 + 2] = ok ? q4.z : 0.f;
-                    v[4 * e4 + 3] = ok ? q4.w : 0.f;
-                }
-                qf[st] = pack_frag<T>(v);
-            }
+            for (int st = 0; st < DS; ++st) kf[t][st] = src[st * (KC * sizeof(E) / 16)];
         }
-        // S: lane holds rows r0 + 4 lg + j, key 16 t + l16
-        f32x4 S[4];
+    }
+    // Value fragments: tile dt holds head dim 16 dt + l16; keys step*KC + EPL*lg .. +EPL.
+    static __device__ __forceinline__ void load_v(const AttnArgs &a, int b, int kvh, int ch, VFrag &vf) {
+        const int lane = threadIdx.x & 63, l16 = lane & 15, lg = lane >> 4;
+        const size_t vt0 = ((size_t)b * a.n_kv + kvh) * HD * a.s_max + (size_t)ch * HD * CK;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+            const E *src = (const E *)a.Vc + vt0 + (16 * dt + l16) * CK + EPL * lg;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) vf[dt][ks] = *(const uint4 *)(src + ks * KC);
+        }
+    }
+    static __device__ __forceinline__ void pack_q(const QRaw &qraw, int r0, int R, uint4 (&qf)[DS]) {
+        const bool ok = r0 + ((threadIdx.x & 63) & 15) < R;
+#pragma unroll
+        for (int st = 0; st < DS; ++st) {
+            float v[EPL];
+#pragma unroll
+            for (int e4 = 0; e4 < EPL / 4; ++e4) {
+                const float4 q4 = qraw[st][e4];
+                v[4 * e4 + 0] = ok ? q4.x : 0.f;
+                v[4 * e4 + 1] = ok ? q4.y : 0.f;
+                v[4 * e4 + 2] = ok ? q4.z : 0.f;
+                v[4 * e4 + 3] = ok ? q4.w : 0.f;
+            }
+            qf[st] = pack_frag<T>(v);
+        }
+    }
+    // S: lane holds rows r0 + 4 lg + j, key 16 t + l16
+    static __device__ __forceinline__ void scores(const uint4 (&qf)[DS], const KFrag &kf, f32x4 (&S)[4]) {
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
             S[t] = (f32x4){0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int st = 0; st < DS; ++st) S[t] = St<T>::mma(qf[st], kf[t][st], S[t]);
         }
+    }
+    // Softmax over the chunk, P through LDS, O = P V, and the row outputs of one tile.  Values of
+    // keys at or past nk have probability zero, but 0 * (NaN or inf) is not, so they are zeroed
+    // as they enter the product (after the softmax, so value loads may still be in flight).
+    template <typename Sink>
+    static __device__ __forceinline__ void finish(const AttnArgs &a, int ch, int len0, int nk, int r0, f32x4 (&S)[4],
+                                                  const VFrag &vf, E (*Ps)[PST], Sink &&sink) {
+        const int lane = threadIdx.x & 63, l16 = lane & 15, lg = lane >> 4;
+        const int kbase = ch * CK;
+        const int G = a.n_heads / a.n_kv, R = a.c * G;
         float rmax[4], rsum[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -719,7 +723,7 @@ __device__ __forceinline__ void attn_chunk(const AttnArgs &a, int b, int kvh, in
         for (int dt = 0; dt < DT; ++dt) {
             f32x4 O = (f32x4){0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) O = St<T>::mma(pf[ks], vf[dt][ks], O);
+            for (int ks = 0; ks < KS; ++ks) O = St<T>::mma(pf[ks], mask_keys<T>(vf[dt][ks], ks * KC + EPL * lg, nk), O);
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const int r = r0 + 4 * lg + j;
@@ -727,6 +731,59 @@ __device__ __forceinline__ void attn_chunk(const AttnArgs &a, int b, int kvh, in
             }
         }
     }
+};
+
+// Any number of query tiles (prefill blocks): the first query tile and the chunk's key and
+// value fragments are all requested before any of them is used; further tiles follow one by one.
+template <DType T, int HD, typename Sink>
+__device__ __forceinline__ void attn_chunk(const AttnArgs &a, int b, int kvh, int ch, int len0, int nk,
+                                           typename St<T>::type (*Ps)[AttnTile<T, HD>::PST], Sink &&sink) {
+    typedef AttnTile<T, HD> A;
+    const int G = a.n_heads / a.n_kv, R = a.c * G;
+    typename A::QRaw qraw;
+    typename A::KFrag kf;
+    typename A::VFrag vf;
+    A::load_q(a, b, kvh, 0, qraw);
+    A::load_k(a, b, kvh, ch, kf);
+    A::load_v(a, b, kvh, ch, vf);
+    // keep every load above in flight before the first use of any of them
+    __builtin_amdgcn_sched_barrier(0);
+    for (int r0 = 0; r0 < R; r0 += 16) {
+        // a tile whose last row sits before this chunk has no keys here (prefill blocks)
+        if (len0 + min(R - 1, r0 + 15) / G < ch * CK) continue;  // uniform across the wave
+        if (r0 > 0) A::load_q(a, b, kvh, r0, qraw);
+        uint4 qf[A::DS];
+        A::pack_q(qraw, r0, R, qf);
+        f32x4 S[4];
+        A::scores(qf, kf, S);
+        A::finish(a, ch, len0, nk, r0, S, vf, Ps, sink);
+    }
+}
+
+// At most 16 query rows (one tile): the values are requested once the scores have consumed the
+// keys, so keys and values are never live together (117 instead of 222 registers at head dim
+// 128 in bf16: four waves per SIMD instead of two), and the value loads overlap the softmax.
+template <DType T, int HD, typename Sink>
+__device__ __forceinline__ void attn_chunk1(const AttnArgs &a, int b, int kvh, int ch, int len0, int nk,
+                                            typename St<T>::type (*Ps)[AttnTile<T, HD>::PST], Sink &&sink) {
+    typedef AttnTile<T, HD> A;
+    const int R = a.c * (a.n_heads / a.n_kv);
+    uint4 qf[A::DS];
+    f32x4 S[4];
+    {
+        typename A::QRaw qraw;
+        typename A::KFrag kf;
+        A::load_q(a, b, kvh, 0, qraw);
+        A::load_k(a, b, kvh, ch, kf);
+        __builtin_amdgcn_sched_barrier(0);
+        A::pack_q(qraw, 0, R, qf);
+        A::scores(qf, kf, S);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    typename A::VFrag vf;
+    A::load_v(a, b, kvh, ch, vf);
+    __builtin_amdgcn_sched_barrier(0);
+    A::finish(a, ch, len0, nk, 0, S, vf, Ps, sink);
 }
 
 // Split-KV decode attention on MFMA: wave w of workgroup x owns chunk WPB x + w of one
@@ -734,8 +791,10 @@ __device__ __forceinline__ void attn_chunk(const AttnArgs &a, int b, int kvh, in
 // agent-scope relaxed stores.  With MERGE, a per-(sequence, kv head) counter then tells the
 // workgroup that finishes last, and that one merges every row's chunks in chunk order, reading
 // them back with coherent (sc1) loads: no cache writeback, and the loads stay in flight together.
-template <DType T, int HD, int WPB, bool MERGE>
-__global__ void __launch_bounds__(64 * WPB) attn_kernel(AttnArgs a) {
+// ONE (at most 16 query rows per kv head) takes attn_chunk1, whose lower register count lets
+// more waves stay resident on the large grids it is used for.
+template <DType T, int HD, int WPB, bool MERGE, bool ONE = false>
+__global__ void __launch_bounds__(64 * WPB, (ONE && T == DType::BF16) ? 3 : 1) attn_kernel(AttnArgs a) {
     typedef typename St<T>::type E;
     constexpr int PST = CK + 16 / (int)sizeof(E);        // padded LDS row of P (elements)
     __shared__ __align__(16) E Ps[WPB][16][PST];
@@ -751,17 +810,19 @@ __global__ void __launch_bounds__(64 * WPB) attn_kernel(AttnArgs a) {
     const int G = a.n_heads / a.n_kv;
     const int R = a.c * G;
     if (ch < nch) {  // uniform across the wave
-        attn_chunk<T, HD>(a, b, kvh, ch, len0, min(CK, pmax + 1 - ch * CK), Ps[w],
-                          [&](int r, int dim, float v, bool stats, float mx, float sm) {
-                              const int i = r / G, gi = r - i * G;
-                              const size_t slot =
-                                  ((size_t)(b * a.c + i) * a.n_heads + kvh * G + gi) * a.chunk_stride + ch;
-                              st_agent(a.part_o + slot * HD + dim, v);
-                              if (stats) {
-                                  st_agent(a.part_ml + slot * 2 + 0, mx);
-                                  st_agent(a.part_ml + slot * 2 + 1, sm);
-                              }
-                          });
+        auto sink = [&](int r, int dim, float v, bool stats, float mx, float sm) {
+            const int i = r / G, gi = r - i * G;
+            const size_t slot = ((size_t)(b * a.c + i) * a.n_heads + kvh * G + gi) * a.chunk_stride + ch;
+            st_agent(a.part_o + slot * HD + dim, v);
+            if (stats) {
+                st_agent(a.part_ml + slot * 2 + 0, mx);
+                st_agent(a.part_ml + slot * 2 + 1, sm);
+            }
+        };
+        if (ONE)
+            attn_chunk1<T, HD>(a, b, kvh, ch, len0, min(CK, pmax + 1 - ch * CK), Ps[w], sink);
+        else
+            attn_chunk<T, HD>(a, b, kvh, ch, len0, min(CK, pmax + 1 - ch * CK), Ps[w], sink);
     }
 
     // Without MERGE, attn_merge_kernel merges in a launch of its own and this workgroup is done.
@@ -811,7 +872,11 @@ static void launch_attention_t(const AttnArgs &a, hipStream_t s, const LaunchEve
         LaunchEvents e1 = ev, e2 = ev;  // one interval around both launches
         e1.stop = nullptr;
         e2.start = nullptr;
-        launch_timed(attn_kernel<T, HD, 4, false>, dim3((a.n_chunks + 3) / 4, a.n_kv, a.B), dim3(256), s, e1, a);
+        if (rows <= 16)  // one query tile: keys and values never live together, more waves resident
+            launch_timed(attn_kernel<T, HD, 4, false, true>, dim3((a.n_chunks + 3) / 4, a.n_kv, a.B), dim3(256), s, e1,
+                         a);
+        else
+            launch_timed(attn_kernel<T, HD, 4, false>, dim3((a.n_chunks + 3) / 4, a.n_kv, a.B), dim3(256), s, e1, a);
         launch_timed(attn_merge_kernel<T, HD>, dim3((all_rows + 3) / 4), dim3(256), s, e2, a);
     } else if (a.c * (a.n_heads / a.n_kv) == 1) {
         launch_timed(attn_kernel<T, HD, 1, true>, dim3(a.n_chunks, a.n_kv, a.B), dim3(64), s, ev, a);
