@@ -791,8 +791,8 @@ __device__ __forceinline__ void attn_chunk1(const AttnArgs &a, int b, int kvh, i
 // agent-scope relaxed stores.  With MERGE, a per-(sequence, kv head) counter then tells the
 // workgroup that finishes last, and that one merges every row's chunks in chunk order, reading
 // them back with coherent (sc1) loads: no cache writeback, and the loads stay in flight together.
-// ONE (at most 16 query rows per kv head) takes attn_chunk1, whose lower register count lets
-// more waves stay resident on the large grids it is used for.
+// ONE (at most 16 query rows per kv head, every decode shape but grouped heads over 16 rows)
+// takes attn_chunk1, whose lower register count lets more waves stay resident.
 template <DType T, int HD, int WPB, bool MERGE, bool ONE = false>
 __global__ void __launch_bounds__(64 * WPB, (ONE && T == DType::BF16) ? 3 : 1) attn_kernel(AttnArgs a) {
     typedef typename St<T>::type E;
@@ -872,14 +872,16 @@ static void launch_attention_t(const AttnArgs &a, hipStream_t s, const LaunchEve
         LaunchEvents e1 = ev, e2 = ev;  // one interval around both launches
         e1.stop = nullptr;
         e2.start = nullptr;
-        if (rows <= 16)  // one query tile: keys and values never live together, more waves resident
+        if (rows <= 16)  // one query tile (attn_chunk1)
             launch_timed(attn_kernel<T, HD, 4, false, true>, dim3((a.n_chunks + 3) / 4, a.n_kv, a.B), dim3(256), s, e1,
                          a);
         else
             launch_timed(attn_kernel<T, HD, 4, false>, dim3((a.n_chunks + 3) / 4, a.n_kv, a.B), dim3(256), s, e1, a);
         launch_timed(attn_merge_kernel<T, HD>, dim3((all_rows + 3) / 4), dim3(256), s, e2, a);
-    } else if (a.c * (a.n_heads / a.n_kv) == 1) {
-        launch_timed(attn_kernel<T, HD, 1, true>, dim3(a.n_chunks, a.n_kv, a.B), dim3(64), s, ev, a);
+    } else if (rows == 1) {
+        launch_timed(attn_kernel<T, HD, 1, true, true>, dim3(a.n_chunks, a.n_kv, a.B), dim3(64), s, ev, a);
+    } else if (rows <= 16) {
+        launch_timed(attn_kernel<T, HD, 4, true, true>, dim3((a.n_chunks + 3) / 4, a.n_kv, a.B), dim3(256), s, ev, a);
     } else {
         launch_timed(attn_kernel<T, HD, 4, true>, dim3((a.n_chunks + 3) / 4, a.n_kv, a.B), dim3(256), s, ev, a);
     }
