@@ -862,12 +862,14 @@ static void launch_attention_t(const AttnArgs &a, hipStream_t s, const LaunchEve
     // One wave per 64-key chunk, four chunks per workgroup: the workgroup that finishes last
     // merges with four waves.  A single query row per kv head over a small grid takes one wave
     // per workgroup instead, which spreads the chunks over more compute units.  A large grid, or
-    // many query rows per kv head (prefill blocks), merges in a second launch instead: otherwise
-    // every workgroup would wait for its partial stores before counting itself done, and the
-    // last merges would run at the kernel's tail, a few waves each merging many rows.
+    // more query rows per kv head than the last workgroup has waves (verify blocks of 6 or more,
+    // grouped-head verify, prefill blocks), merges in a second launch instead, one wave per row:
+    // otherwise every workgroup would wait for its partial stores before counting itself done,
+    // and the last merges would run at the kernel's tail, each wave merging several rows one
+    // after another (6 rows: 17.1 -> 16.0 us, 20 rows: 18.6 -> 15.7 us with the second launch).
     const long waves = (long)a.n_chunks * a.n_kv * a.B;
     const int rows = a.c * (a.n_heads / a.n_kv);
-    if (waves >= kAttnLargeGrid || rows > 32) {
+    if (waves >= kAttnLargeGrid || rows > 4) {
         const int all_rows = a.B * a.c * a.n_heads;
         LaunchEvents e1 = ev, e2 = ev;  // one interval around both launches
         e1.stop = nullptr;
@@ -880,10 +882,8 @@ static void launch_attention_t(const AttnArgs &a, hipStream_t s, const LaunchEve
         launch_timed(attn_merge_kernel<T, HD>, dim3((all_rows + 3) / 4), dim3(256), s, e2, a);
     } else if (rows == 1) {
         launch_timed(attn_kernel<T, HD, 1, true, true>, dim3(a.n_chunks, a.n_kv, a.B), dim3(64), s, ev, a);
-    } else if (rows <= 16) {
-        launch_timed(attn_kernel<T, HD, 4, true, true>, dim3((a.n_chunks + 3) / 4, a.n_kv, a.B), dim3(256), s, ev, a);
     } else {
-        launch_timed(attn_kernel<T, HD, 4, true>, dim3((a.n_chunks + 3) / 4, a.n_kv, a.B), dim3(256), s, ev, a);
+        launch_timed(attn_kernel<T, HD, 4, true, true>, dim3((a.n_chunks + 3) / 4, a.n_kv, a.B), dim3(256), s, ev, a);
     }
 }
 
