@@ -259,6 +259,16 @@ static void launch_gemm_big(Epi e, const GemmArgs &a, hipStream_t s, const Launc
 struct GemmShape {
     int rt, waves;
 };
+static int compute_units() {
+    static const int cu = [] {
+        int dev = 0, v = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0)
+            v = 256;
+        return v;
+    }();
+    return cu;
+}
 static GemmShape gemm_shape(int N, int K, int KC, int M) {
     const int tiles = N / 16, chunks = K / KC, mg = (M + 15) / 16;
     // K split, from the matrix only: the most waves per workgroup (up to 16) that keep the whole
@@ -273,6 +283,14 @@ static GemmShape gemm_shape(int N, int K, int KC, int M) {
         if (mg >= 3 && tiles % 4 == 0) rt = 4;
         else if (mg >= 2 && tiles % 2 == 0) rt = 2;
         while (rt > w) rt >>= 1;
+        // Workgroups this wide hold one compute unit's share of registers per 8 waves, so the
+        // grid runs in rounds of (CUs x 8 / w) workgroups: take 3 tiles instead of 4 when that
+        // needs fewer tile-rounds (QKV at 7B: 256 workgroups, one full round, instead of 192).
+        if (rt == 4 && tiles % 3 == 0) {
+            const long slots = (long)compute_units() * 8 / w;
+            auto cost = [&](int r) { return ((tiles / r + slots - 1) / slots) * r; };
+            if (cost(3) < cost(4)) rt = 3;
+        }
     }
     return {rt, w};
 }
@@ -317,6 +335,7 @@ static void gemm_dispatch(Epi e, const GemmArgs &a, GemmShape sh, hipStream_t s,
     }
     switch (sh.rt) {
         case 4: gemm_dispatch_epi<T, 4, 8>(e, a, grid, block, s, ev); break;
+        case 3: gemm_dispatch_epi<T, 3, 8>(e, a, grid, block, s, ev); break;
         case 2: gemm_dispatch_epi<T, 2, 8>(e, a, grid, block, s, ev); break;
         default: gemm_dispatch_epi<T, 1, 8>(e, a, grid, block, s, ev); break;
     }
