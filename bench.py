@@ -205,6 +205,8 @@ def main():
     ver_gbs = float(np.mean(st["verify_bytes"])) / (ver_ms * 1e-3) / 1e9
     dr_ms = float(np.median(st["draft_ms"]))
     dr_gbs = float(np.mean(st["draft_bytes"])) / (dr_ms * 1e-3) / 1e9
+    step_bytes = float(np.mean(st["draft_bytes"])) + float(np.mean(st["verify_bytes"]))
+    step_gbs = step_bytes / (ms_step * 1e-3) / 1e9
     log("timed %d steps: %.1f tokens/s, %.2f ms/step, mean m %.2f, verify %.3f ms (%.0f GB/s), "
         "draft %.3f ms (%.0f GB/s)" % (K, value, ms_step, mv.mean(), ver_ms, ver_gbs, dr_ms, dr_gbs))
     # drafter update (the workloads that train the drafter): its dense work is the LoRA head
@@ -335,6 +337,11 @@ def main():
         "verify_step": {"ms": round(ver_ms, 4), "gb_s": round(ver_gbs, 1), "frac": round(ver_gbs / HBM_PEAK_GBS, 4),
                         "bytes": int(np.mean(st["verify_bytes"]))},
         "draft_token": {"ms": round(dr_ms / k, 4), "gb_s": round(dr_gbs, 1), "frac": round(dr_gbs / HBM_PEAK_GBS, 4)},
+        # the whole step (k_spec draft passes + verify, wall time of the timed loop): its frac is
+        # also committed tokens/s over the rate the same bytes would allow at the HBM peak
+        "step": {"ms": round(ms_step, 4), "bytes": int(step_bytes), "gb_s": round(step_gbs, 1),
+                 "frac": round(step_gbs / HBM_PEAK_GBS, 4),
+                 "tokens_per_s_at_peak": round(float(nv.mean()) * B / (step_bytes / (HBM_PEAK_GBS * 1e9)), 1)},
         "acceptance": {"mean_m": round(float(mv.mean()), 4), "mean_tokens_per_step": round(float(nv.mean()), 4),
                        "rate": round(float(mv.mean()) / k, 4)},
         "ar_baseline": ar,
