@@ -476,6 +476,49 @@ def test_sampled_drafts_match_oracle(name, tau):
     eng.close()
 
 
+def test_sampled_drafts_use_each_sequences_own_counter_row():
+    """At batch 3, sequence b's draws come from counter row b * 16 + j: its drafts are the
+    oracle's draws for sequence index b (wherever the oracle's perturbed scores are not near a
+    tie), and every sequence's commits stay greedy decoding's."""
+    shape = gu.SHAPES["tiny"]
+    B, P, T, k, seed, tau = 3, 24, 30, 4, 17, 1.0
+    w = synth.make_weights(shape, 0, lora_A_std=0.05)
+    prompts = synth.make_prompts(shape.vocab, B, P, 8)
+    om = oracle.OracleModel(w)
+    refs = [odvi.dvi_generate(om, prompts[b], T, k,
+                              odvi.Drafter(w.lora_A.astype(np.float64), w.lora_B.astype(np.float64), shape.lora_gamma,
+                                           sample_tau=tau, seed=seed, seq=b)) for b in range(B)]
+    eng, _ = gu.engine(shape, max_batch=B, max_seq=P + T + 16, weights=w)
+    eng.set_sampling(tau, seed)
+    first = eng.prefill(prompts)
+    out = [[int(first[b])] for b in range(B)]
+    live = [True] * B
+    agree, step = 0, 0
+    while min(len(o) for o in out) < T:
+        remaining = np.array([T - len(o) for o in out], np.int32)
+        d = eng.draft(k, want=True)
+        eng.verify()
+        tok, n, m = eng.commit(max_new=remaining)
+        for b in range(B):
+            if remaining[b] > 0 and live[b] and step < len(refs[b].steps):
+                st = refs[b].steps[step]
+                for j in range(k):
+                    if st.draft_gaps[j] <= 1e-3:
+                        live[b] = False
+                        break
+                    assert d[b, j] == st.drafts[j], (b, step, d[b], st.drafts)
+                    agree += 1
+                if live[b]:
+                    assert (m[b], n[b]) == (st.m, st.n), (b, step)
+            out[b].extend(int(t) for t in tok[b, :n[b]])
+        step += 1
+    for b in range(B):
+        assert np.array_equal(np.array(out[b]), refs[b].tokens), b
+    _say("per-sequence sampled drafts: %d drafts equal to the oracle's draws" % agree)
+    assert agree >= 3 * k
+    eng.close()
+
+
 def test_sampled_drafting_is_lossless_and_changes_drafts():
     """With sampled drafts, speculative decoding still equals greedy decoding bitwise (tokens
     and keys/values); the accept lengths differ from argmax drafting."""
