@@ -179,6 +179,25 @@ dvi_status dvi_verify(dvi_ctx *ctx, int32_t *targets_out, int32_t *accept_out);
 dvi_status dvi_commit(dvi_ctx *ctx, const int32_t *max_new, const int32_t *forced_commit, int32_t *tokens_out,
                       int32_t *n_out, int32_t *accept_out);
 
+/*
+ * Several decode steps in one call (Section 3.3, the draft -> verify -> commit -> log loop):
+ * n_steps (1..64) steps of dvi_draft + dvi_verify + dvi_commit with k_spec drafts each,
+ * queued on the stream without a host synchronisation between them; each sequence's
+ * remaining-token count lives on the device and the commit kernel lowers it, so a sequence
+ * that reaches its max_new commits nothing further (its lanes keep computing).  Results are
+ * those of n_steps separate calls, bit for bit.  max_new: NULL (no limit) or HOST int32
+ * [batch].  tokens_out: HOST int32 [n_steps, batch, k_spec] (entries past n are -1); n_out:
+ * HOST int32 [n_steps, batch]; accept_out: NULL or HOST int32 [n_steps, batch] receiving m.
+ * No drafter update runs inside; callers that train the drafter call dvi_update_drafter
+ * between calls.  The capacity check is made up front on the longest length the steps could
+ * reach (each sequence grows by at most min(k_spec per step, max_new)): DVI_ERR_CAPACITY
+ * if any could pass max_seq.  DVI_ERR_NUMERIC if a head produced a non-finite logit: nothing
+ * is committed from that step on, the earlier steps stand, and the context is READY.
+ * READY -> READY
+ */
+dvi_status dvi_decode_steps(dvi_ctx *ctx, int32_t k_spec, int32_t n_steps, const int32_t *max_new,
+                            int32_t *tokens_out, int32_t *n_out, int32_t *accept_out);
+
 /* Return to the last committed state from DRAFTED or VERIFIED (length reset only). */
 dvi_status dvi_abort_step(dvi_ctx *ctx);
 

@@ -52,6 +52,7 @@ SIGNATURES = {
     "dvi_draft": (c_i32, [c_vp, c_i32, c_vp, c_vp]),
     "dvi_verify": (c_i32, [c_vp, c_vp, c_vp]),
     "dvi_commit": (c_i32, [c_vp, c_vp, c_vp, c_vp, c_vp, c_vp]),
+    "dvi_decode_steps": (c_i32, [c_vp, c_i32, c_i32, c_vp, c_vp, c_vp, c_vp]),
     "dvi_abort_step": (c_i32, [c_vp]),
     "dvi_update_drafter": (c_i32, [c_vp, ctypes.POINTER(UpdateArgs), ctypes.POINTER(UpdateStats)]),
     "dvi_last_error": (ctypes.c_char_p, [c_vp]),

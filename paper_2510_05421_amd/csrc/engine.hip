@@ -9,6 +9,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
 #include <array>
 #include <map>
 #include <vector>
@@ -21,6 +22,7 @@ using namespace dvi;
 namespace {
 
 constexpr int kMaxRows = 64;   // rows of a decode-step GEMM (four 16-wide MFMA groups)
+constexpr int kMaxDecodeSteps = 64;  // steps one dvi_decode_steps call may queue
 
 enum State { S_CREATED = 0, S_READY, S_DRAFTED, S_VERIFIED };
 
@@ -71,6 +73,7 @@ struct dvi_ctx {
     int32_t *lens, *pending, *drafts, *targets, *forced, *max_new, *ids, *copy_list, *ring_state;
     int32_t *rng_step;  // [0]: decode steps committed since the prefill (the sampling counter)
     int32_t *io;  // [0,B*k) tokens | [B*k, B*k+B) n | [.., +B) m | flags[4]
+    int32_t *steps_io;  // dvi_decode_steps: tokens [steps][B][k] | n [steps][B] | m [steps][B]
     int32_t *prow;
     // replay ring
     void *ring_h;
@@ -208,6 +211,7 @@ static size_t layout(dvi_ctx *x, const dvi_config &c, void *base) {
     int32_t *ring_state = b.take<int32_t>(4 * 4);
     int32_t *rng_step = b.take<int32_t>(4 * 4);
     int32_t *io = b.take<int32_t>((Bk + 2 * c.max_batch + 4) * 4);
+    int32_t *steps_io = b.take<int32_t>((size_t)kMaxDecodeSteps * (Bk + 2 * c.max_batch) * 4);
     size_t maxN = V;
     if ((size_t)qkv_rows(c) > maxN) maxN = qkv_rows(c);
     if (2 * F > maxN) maxN = 2 * F;
@@ -241,6 +245,7 @@ static size_t layout(dvi_ctx *x, const dvi_config &c, void *base) {
         x->att_po = att_po; x->att_pml = att_pml; x->att_cnt = att_cnt; x->chunk_stride = (int)cs;
         x->lens = lens; x->pending = pending; x->drafts = drafts; x->targets = targets; x->forced = forced;
         x->max_new = max_new; x->ids = ids; x->copy_list = copy_list; x->ring_state = ring_state; x->rng_step = rng_step; x->io = io;
+        x->steps_io = steps_io;
         x->prow = prow;
         x->ring_h = ring_h; x->ring_logits = ring_logits; x->ring_a = ring_a; x->ring_i = ring_i;
         x->ring_prev = ring_prev; x->ring_r = ring_r; x->ring_fresh = ring_fresh;
@@ -748,29 +753,13 @@ extern "C" dvi_status dvi_prefill(dvi_ctx *x, int32_t batch, const int32_t *ids,
     return DVI_OK;
 }
 
-extern "C" dvi_status dvi_draft(dvi_ctx *x, int32_t k_spec, const int32_t *forced, int32_t *drafts_out) {
-    if (!x) return DVI_ERR_ARG;
-    if (x->device_error) return fail(x, DVI_ERR_DEVICE, "context has a sticky device error");
-    if (x->state != S_READY) return fail(x, DVI_ERR_STATE, "draft needs state READY");
+// One draft pass (Section 3.3): k_spec serial single-token passes of layers 1..k from the
+// pending tokens, each followed by the draft head (or, in plain decoding, by nothing).
+static dvi_status draft_pass(dvi_ctx *x, int k_spec, bool forced, int nck) {
     const dvi_config &cf = x->cfg;
-    if (k_spec < 1) return fail(x, DVI_ERR_ARG, "k_spec < 1");
-    if (k_spec > cf.max_k_spec) return fail(x, DVI_ERR_CAPACITY, "k_spec %d > max_k_spec %d", k_spec, cf.max_k_spec);
-    for (int b = 0; b < x->B; ++b)
-        if (x->lens_h[b] + k_spec > cf.max_seq)
-            return fail(x, DVI_ERR_CAPACITY, "sequence %d: length %d + k_spec %d > max_seq %d", b, x->lens_h[b], k_spec,
-                        cf.max_seq);
-    const int B = x->B, d = cf.d_model;
-    if (forced) {
-        for (int i = 0; i < B * k_spec; ++i)
-            if (forced[i] < 0 || forced[i] >= cf.vocab) return fail(x, DVI_ERR_ARG, "forced draft id out of range");
-        HIPCHK(x, hipMemcpyAsync(x->forced, forced, (size_t)B * k_spec * 4, hipMemcpyHostToDevice, x->stream));
-    }
-    ev_begin(x, 0);
-    HIPCHK(x, hipMemsetAsync(flags_ptr(x), 0, 16, x->stream));
+    const int B = x->B, d = cf.d_model, nps = d / 16;
     x->ar_mode = (k_spec == 1 && !forced) ? 1 : 0;
-    const int nps = d / 16;
-    const int nck = attn_chunks(x, max_len(x) + k_spec - 1);
-    const dvi_status st = run_pass(x, {0, B, k_spec, x->ar_mode + 2 * (forced != nullptr), nck}, [&]() -> dvi_status {
+    const dvi_status st = run_pass(x, {0, B, k_spec, x->ar_mode + 2 * (forced ? 1 : 0), nck}, [&]() -> dvi_status {
         for (int j = 0; j < k_spec; ++j) {
             // draft token j of sequence b lives in row b*k_spec + j of hk / hk_ss / hk_hg
             const int32_t *tok = j == 0 ? x->pending : x->drafts + (j - 1);
@@ -794,9 +783,89 @@ extern "C" dvi_status dvi_draft(dvi_ctx *x, int32_t k_spec, const int32_t *force
     });
     if (st != DVI_OK) return st;
     if (x->ar_mode) HIPCHK(x, hipMemsetAsync(x->drafts, 0xff, (size_t)B * 4, x->stream));
-    ev_end(x, 0);
     LAUNCHCHK(x);
     x->k_spec = k_spec;
+    return DVI_OK;
+}
+
+// One verify pass (Section 3.3): layers k+1..L over the B * k_spec kept rows, then the head.
+static dvi_status verify_pass(dvi_ctx *x, int nck) {
+    const dvi_config &cf = x->cfg;
+    const int B = x->B, k = x->k_spec, M = B * k, d = cf.d_model;
+    const dvi_status st = run_pass(x, {1, B, k, 0, nck}, [&]() -> dvi_status {
+        dvi_status sl =
+            run_layers(x, cf.split_k, cf.n_layers, B, k, 0, nck, x->hk, x->hk_ss, x->hk_hg, 1, x->hk_hg, 1, 0);
+        if (sl != DVI_OK) return sl;
+        head(x, x->hk_hg, x->hk_ss, d / 16, M, x->vlogits, false, x->targets, 1, nullptr);
+        LAUNCHCHK(x);
+        return DVI_OK;
+    });
+    if (st != DVI_OK) return st;
+    LAUNCHCHK(x);
+    return DVI_OK;
+}
+
+// The commit kernel and the ring copy of the rows it logs.  limit: x->max_new holds each
+// sequence's remaining tokens; dec: the kernel subtracts what it commits (several steps in a row).
+static dvi_status commit_launch(dvi_ctx *x, bool limit, bool dec, int32_t *tok, int32_t *n, int32_t *m) {
+    const dvi_config &cf = x->cfg;
+    const int B = x->B, k = x->k_spec;
+    CommitArgs a{};
+    a.B = B;
+    a.k_spec = k;
+    a.drafts = x->drafts;
+    a.targets = x->targets;
+    a.max_new = limit ? x->max_new : nullptr;
+    a.max_new_dec = dec ? 1 : 0;
+    a.lens = x->lens;
+    a.pending = x->pending;
+    a.tokens_out = tok;
+    a.n_out = n;
+    a.m_out = m;
+    a.flags = flags_ptr(x);
+    a.ring_state = x->ring_state;
+    a.ring_rows = x->ar_mode ? 0 : cf.buffer_rows;
+    a.copy_list = x->copy_list;
+    a.ring_a = x->ring_a;
+    a.ring_i = x->ring_i;
+    a.ring_prev = x->ring_prev;
+    a.ring_r = x->ring_r;
+    a.ring_fresh = x->ring_fresh;
+    a.rng_step = x->rng_step;
+    if (x->ar_mode) {
+        // plain autoregressive step: nothing was drafted; commit y*_1 only
+        HIPCHK(x, hipMemsetAsync(x->drafts, 0xff, (size_t)B * 4, x->stream));
+    }
+    launch_commit(a, x->stream);
+    if (!x->ar_mode)
+        launch_ring_copy(x->copy_list, B * k, x->hk_hat, cf.d_model, (int)x->es, x->vlogits, cf.vocab, x->ring_h,
+                         x->ring_logits, x->stream);
+    LAUNCHCHK(x);
+    return DVI_OK;
+}
+
+extern "C" dvi_status dvi_draft(dvi_ctx *x, int32_t k_spec, const int32_t *forced, int32_t *drafts_out) {
+    if (!x) return DVI_ERR_ARG;
+    if (x->device_error) return fail(x, DVI_ERR_DEVICE, "context has a sticky device error");
+    if (x->state != S_READY) return fail(x, DVI_ERR_STATE, "draft needs state READY");
+    const dvi_config &cf = x->cfg;
+    if (k_spec < 1) return fail(x, DVI_ERR_ARG, "k_spec < 1");
+    if (k_spec > cf.max_k_spec) return fail(x, DVI_ERR_CAPACITY, "k_spec %d > max_k_spec %d", k_spec, cf.max_k_spec);
+    for (int b = 0; b < x->B; ++b)
+        if (x->lens_h[b] + k_spec > cf.max_seq)
+            return fail(x, DVI_ERR_CAPACITY, "sequence %d: length %d + k_spec %d > max_seq %d", b, x->lens_h[b], k_spec,
+                        cf.max_seq);
+    const int B = x->B;
+    if (forced) {
+        for (int i = 0; i < B * k_spec; ++i)
+            if (forced[i] < 0 || forced[i] >= cf.vocab) return fail(x, DVI_ERR_ARG, "forced draft id out of range");
+        HIPCHK(x, hipMemcpyAsync(x->forced, forced, (size_t)B * k_spec * 4, hipMemcpyHostToDevice, x->stream));
+    }
+    ev_begin(x, 0);
+    HIPCHK(x, hipMemsetAsync(flags_ptr(x), 0, 16, x->stream));
+    const dvi_status st = draft_pass(x, k_spec, forced != nullptr, attn_chunks(x, max_len(x) + k_spec - 1));
+    if (st != DVI_OK) return st;
+    ev_end(x, 0);
     if (drafts_out) {
         HIPCHK(x, hipMemcpyAsync(drafts_out, x->drafts, (size_t)B * k_spec * 4, hipMemcpyDeviceToHost, x->stream));
         HIPCHK(x, hipStreamSynchronize(x->stream));
@@ -809,21 +878,11 @@ extern "C" dvi_status dvi_verify(dvi_ctx *x, int32_t *targets_out, int32_t *acce
     if (!x) return DVI_ERR_ARG;
     if (x->device_error) return fail(x, DVI_ERR_DEVICE, "context has a sticky device error");
     if (x->state != S_DRAFTED) return fail(x, DVI_ERR_STATE, "verify needs state DRAFTED");
-    const dvi_config &cf = x->cfg;
-    const int B = x->B, k = x->k_spec, M = B * k, d = cf.d_model;
+    const int B = x->B, k = x->k_spec, M = B * k;
     ev_begin(x, 1);
-    const int nck = attn_chunks(x, max_len(x) + k - 1);
-    const dvi_status st = run_pass(x, {1, B, k, 0, nck}, [&]() -> dvi_status {
-        dvi_status sl =
-            run_layers(x, cf.split_k, cf.n_layers, B, k, 0, nck, x->hk, x->hk_ss, x->hk_hg, 1, x->hk_hg, 1, 0);
-        if (sl != DVI_OK) return sl;
-        head(x, x->hk_hg, x->hk_ss, d / 16, M, x->vlogits, false, x->targets, 1, nullptr);
-        LAUNCHCHK(x);
-        return DVI_OK;
-    });
+    const dvi_status st = verify_pass(x, attn_chunks(x, max_len(x) + k - 1));
     if (st != DVI_OK) return st;
     ev_end(x, 1);
-    LAUNCHCHK(x);
     if (targets_out || accept_out) {
         std::vector<int32_t> tg((size_t)M), dr((size_t)M);
         HIPCHK(x, hipMemcpyAsync(tg.data(), x->targets, (size_t)M * 4, hipMemcpyDeviceToHost, x->stream));
@@ -863,37 +922,9 @@ extern "C" dvi_status dvi_commit(dvi_ctx *x, const int32_t *max_new, const int32
         HIPCHK(x, hipMemcpyAsync(x->max_new, max_new, (size_t)B * 4, hipMemcpyHostToDevice, x->stream));
     }
     ev_begin(x, 2);
-    CommitArgs a{};
-    a.B = B;
-    a.k_spec = k;
-    a.drafts = x->drafts;
-    a.targets = x->targets;
-    a.max_new = max_new ? x->max_new : nullptr;
-    a.lens = x->lens;
-    a.pending = x->pending;
-    a.tokens_out = x->io;
-    a.n_out = x->io + io_n(x);
-    a.m_out = x->io + io_m(x);
-    a.flags = flags_ptr(x);
-    a.ring_state = x->ring_state;
-    a.ring_rows = x->ar_mode ? 0 : cf.buffer_rows;
-    a.copy_list = x->copy_list;
-    a.ring_a = x->ring_a;
-    a.ring_i = x->ring_i;
-    a.ring_prev = x->ring_prev;
-    a.ring_r = x->ring_r;
-    a.ring_fresh = x->ring_fresh;
-    a.rng_step = x->rng_step;
-    if (x->ar_mode) {
-        // plain autoregressive step: nothing was drafted; commit y*_1 only
-        HIPCHK(x, hipMemsetAsync(x->drafts, 0xff, (size_t)B * 4, x->stream));
-    }
-    launch_commit(a, x->stream);
-    if (!x->ar_mode)
-        launch_ring_copy(x->copy_list, B * k, x->hk_hat, cf.d_model, (int)x->es, x->vlogits, cf.vocab, x->ring_h,
-                         x->ring_logits, x->stream);
+    const dvi_status st = commit_launch(x, max_new != nullptr, false, x->io, x->io + io_n(x), x->io + io_m(x));
+    if (st != DVI_OK) return st;
     ev_end(x, 2);
-    LAUNCHCHK(x);
     std::vector<int32_t> io((size_t)io_words(x));
     HIPCHK(x, hipMemcpyAsync(io.data(), x->io, io.size() * 4, hipMemcpyDeviceToHost, x->stream));
     HIPCHK(x, hipStreamSynchronize(x->stream));
@@ -912,6 +943,67 @@ extern "C" dvi_status dvi_commit(dvi_ctx *x, const int32_t *max_new, const int32
         }
     }
     x->state = S_READY;
+    return DVI_OK;
+}
+
+extern "C" dvi_status dvi_decode_steps(dvi_ctx *x, int32_t k_spec, int32_t n_steps, const int32_t *max_new,
+                                       int32_t *tokens_out, int32_t *n_out, int32_t *accept_out) {
+    if (!x) return DVI_ERR_ARG;
+    if (x->device_error) return fail(x, DVI_ERR_DEVICE, "context has a sticky device error");
+    if (x->state != S_READY) return fail(x, DVI_ERR_STATE, "decode_steps needs state READY");
+    if (!tokens_out || !n_out) return fail(x, DVI_ERR_ARG, "null output");
+    const dvi_config &cf = x->cfg;
+    const int B = x->B;
+    if (k_spec < 1) return fail(x, DVI_ERR_ARG, "k_spec < 1");
+    if (k_spec > cf.max_k_spec) return fail(x, DVI_ERR_CAPACITY, "k_spec %d > max_k_spec %d", k_spec, cf.max_k_spec);
+    if (n_steps < 1 || n_steps > kMaxDecodeSteps)
+        return fail(x, DVI_ERR_ARG, "n_steps %d outside 1..%d", n_steps, kMaxDecodeSteps);
+    if (max_new)
+        for (int b = 0; b < B; ++b)
+            if (max_new[b] < 0) return fail(x, DVI_ERR_ARG, "max_new < 0");
+    // A sequence grows by at most k_spec per step and by at most its max_new in all; each step's
+    // drafts write k_spec positions past the length it starts from.
+    auto grown = [&](int b, int steps) {
+        const long g = (long)steps * k_spec;
+        return (int)(max_new && max_new[b] < g ? max_new[b] : g);
+    };
+    for (int b = 0; b < B; ++b)
+        if (x->lens_h[b] + grown(b, n_steps - 1) + k_spec > cf.max_seq)
+            return fail(x, DVI_ERR_CAPACITY, "sequence %d: length %d may reach %d after %d steps of %d > max_seq %d", b,
+                        x->lens_h[b], x->lens_h[b] + grown(b, n_steps - 1) + k_spec, n_steps, k_spec, cf.max_seq);
+    if (max_new) HIPCHK(x, hipMemcpyAsync(x->max_new, max_new, (size_t)B * 4, hipMemcpyHostToDevice, x->stream));
+    HIPCHK(x, hipMemsetAsync(flags_ptr(x), 0, 16, x->stream));
+    const int Bk = B * k_spec;
+    int32_t *tok_d = x->steps_io, *n_d = tok_d + (size_t)n_steps * Bk, *m_d = n_d + (size_t)n_steps * B;
+    for (int st = 0; st < n_steps; ++st) {
+        // the attention grid covers the longest length this step can start from
+        int pmax = 0;
+        for (int b = 0; b < B; ++b) pmax = std::max(pmax, x->lens_h[b] + grown(b, st));
+        const int nck = attn_chunks(x, pmax + k_spec - 1);
+        dvi_status s = draft_pass(x, k_spec, false, nck);
+        if (s == DVI_OK) s = verify_pass(x, nck);
+        if (s == DVI_OK)
+            s = commit_launch(x, max_new != nullptr, true, tok_d + (size_t)st * Bk, n_d + (size_t)st * B,
+                              m_d + (size_t)st * B);
+        if (s != DVI_OK) return s;
+    }
+    std::vector<int32_t> io((size_t)n_steps * (Bk + 2 * B)), fl(4), rs(4);
+    HIPCHK(x, hipMemcpyAsync(io.data(), x->steps_io, io.size() * 4, hipMemcpyDeviceToHost, x->stream));
+    HIPCHK(x, hipMemcpyAsync(fl.data(), flags_ptr(x), 16, hipMemcpyDeviceToHost, x->stream));
+    HIPCHK(x, hipMemcpyAsync(rs.data(), x->ring_state, 16, hipMemcpyDeviceToHost, x->stream));
+    HIPCHK(x, hipStreamSynchronize(x->stream));
+    const int32_t *tok = io.data(), *nn = tok + (size_t)n_steps * Bk, *mm = nn + (size_t)n_steps * B;
+    memcpy(tokens_out, tok, (size_t)n_steps * Bk * 4);
+    memcpy(n_out, nn, (size_t)n_steps * B * 4);
+    if (accept_out) memcpy(accept_out, mm, (size_t)n_steps * B * 4);
+    // host mirrors of the lengths and of the ring's valid rows
+    for (int st = 0; st < n_steps; ++st)
+        for (int b = 0; b < B; ++b) x->lens_h[b] += nn[(size_t)st * B + b];
+    x->ring_valid_h = rs[1];
+    x->state = S_READY;
+    // Non-finite logits: the commit kernel commits nothing from that step on; the earlier steps
+    // stand, and the context stays usable from the lengths they reached.
+    if (fl[0]) return fail(x, DVI_ERR_NUMERIC, "non-finite logits in the draft or verify head");
     return DVI_OK;
 }
 

@@ -141,7 +141,8 @@ struct CommitArgs {
     int B, k_spec;
     const int32_t *drafts;    // [B][k_spec]
     const int32_t *targets;   // [B][k_spec]
-    const int32_t *max_new;   // [B] or nullptr
+    int32_t *max_new;         // [B] or nullptr: tokens each sequence may still commit
+    int max_new_dec;          // 1: subtract each sequence's n from max_new (several steps in a row)
     int32_t *lens, *pending;  // [B]
     int32_t *tokens_out;      // [B][k_spec]
     int32_t *n_out, *m_out;   // [B]

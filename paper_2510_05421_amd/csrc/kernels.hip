@@ -1008,6 +1008,7 @@ __global__ void __launch_bounds__(64) commit_kernel(CommitArgs a) {
         if (n > 0) a.pending[b] = tg[n - 1];
         a.n_out[b] = n;
         a.m_out[b] = m;
+        if (a.max_new && a.max_new_dec) a.max_new[b] = lim - n;
         rows = (lim > 0 && a.ring_rows > 0) ? min(m + 1, k) : 0;
     }
     // inclusive prefix sum of the row counts over the lanes (sequence order)

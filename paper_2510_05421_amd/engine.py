@@ -207,6 +207,18 @@ class Engine:
                                         tok.ctypes.data, n.ctypes.data, m.ctypes.data))
         return tok, n, m
 
+    def decode_steps(self, k_spec: int, n_steps: int, max_new=None):
+        """n_steps draft/verify/commit steps in one call (no host sync between them): tokens
+        [n_steps, batch, k_spec] (-1 past n), n [n_steps, batch], m [n_steps, batch]."""
+        tok = np.empty((n_steps, self.batch, k_spec), np.int32)
+        n = np.empty((n_steps, self.batch), np.int32)
+        m = np.empty((n_steps, self.batch), np.int32)
+        mx = _i32(max_new) if max_new is not None else None
+        self._check(self.lib.dvi_decode_steps(self.ctx, k_spec, n_steps, mx.ctypes.data if mx is not None else None,
+                                              tok.ctypes.data, n.ctypes.data, m.ctypes.data))
+        self.k_spec = k_spec
+        return tok, n, m
+
     def abort(self):
         self._check(self.lib.dvi_abort_step(self.ctx))
 

@@ -80,6 +80,7 @@ def test_create_argument_errors_need_no_gpu():
     assert lib.dvi_abort_step(None) == _abi.ERR_ARG
     assert lib.dvi_set_graphs(None, 1) == _abi.ERR_ARG
     assert lib.dvi_set_sampling(None, 1.0, 3) == _abi.ERR_ARG
+    assert lib.dvi_decode_steps(None, 4, 8, None, None, None, None) == _abi.ERR_ARG
     assert lib.dvi_last_error(None) == b"null context"
 
 

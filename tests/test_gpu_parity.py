@@ -519,6 +519,63 @@ def test_sampled_drafts_use_each_sequences_own_counter_row():
     eng.close()
 
 
+@pytest.mark.parametrize("name,B,k,tau", [("tiny", 3, 4, 0.0), ("1b_L4", 2, 5, 0.0), ("tiny", 2, 4, 1.0),
+                                          ("tiny", 2, 1, 0.0)])
+def test_decode_steps_equal_separate_calls(name, B, k, tau):
+    """Steps queued by dvi_decode_steps (no host synchronisation between them, remaining-token
+    limits kept on the device) give the tokens, accept lengths, lengths, caches and replay ring
+    of the same steps as separate draft/verify/commit calls, bit for bit, including a sequence
+    that reaches its limit in the middle of a call."""
+    shape = gu.SHAPES[name]
+    P, S = 20, 12
+    prompts = synth.make_prompts(shape.vocab, B, P, 13)
+    w = synth.make_weights(shape, 0, lora_A_std=0.03)
+    limits = np.array([S * k, 5, 17][:B], np.int32)
+
+    def run(multi):
+        eng, _ = gu.engine(shape, max_batch=B, max_seq=P + S * k + 16, weights=w, buffer_rows=64)
+        if tau > 0:
+            eng.set_sampling(tau, 5)
+        eng.prefill(prompts)
+        left = limits.copy()
+        toks, ns, ms = [], [], []
+        if multi:
+            for cnt in (5, S - 5):
+                t, n, m = eng.decode_steps(k, cnt, max_new=left)
+                toks += list(t)
+                ns += list(n)
+                ms += list(m)
+                left = left - n.sum(axis=0)
+        else:
+            for _ in range(S):
+                eng.draft(k)
+                eng.verify()
+                t, n, m = eng.commit(max_new=left)
+                toks.append(t)
+                ns.append(n)
+                ms.append(m)
+                left = left - n
+        lens = eng.lengths()
+        kv = [eng.read_kv(l, b, 0, int(lens[b])) for l in (0, shape.n_layers - 1) for b in range(B)]
+        valid, nxt = eng.buffer_info()
+        ring = eng.read_buffer(0, valid) if valid else None
+        eng.close()
+        return np.array(toks), np.array(ns), np.array(ms), lens, kv, (valid, nxt), ring
+
+    a_ = run(False)
+    b_ = run(True)
+    for x, y in zip(a_[:4], b_[:4]):
+        assert np.array_equal(x, y)
+    assert np.array_equal(a_[1].sum(axis=0), np.minimum(limits, a_[1].sum(axis=0)))
+    assert int(a_[1][:, 1].sum()) == 5  # the second sequence stops at its limit
+    for (k1, v1), (k2, v2) in zip(a_[4], b_[4]):
+        assert np.array_equal(k1, k2) and np.array_equal(v1, v2)
+    assert a_[5] == b_[5]
+    if a_[6] is not None:
+        for key in a_[6]:
+            assert np.array_equal(a_[6][key], b_[6][key]), key
+
+
 def test_sampled_drafting_is_lossless_and_changes_drafts():
     """With sampled drafts, speculative decoding still equals greedy decoding bitwise (tokens
     and keys/values); the accept lengths differ from argmax drafting."""
