@@ -94,6 +94,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=30.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-ar", action="store_true")
+    ap.add_argument("--no-device-steps", action="store_true",
+                    help="skip the leg that runs the decode loop through dvi_decode_steps")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="first run 3 plain device-to-device copies of this many MiB (a reference for "
                          "the hardware byte counters under a profiler)")
@@ -143,6 +145,16 @@ def main():
     remaining = np.full(B, N - 1, np.int32)
     state = {"step": 0}
 
+    def update_drafter(stats=None):
+        c = sched.coeffs(eng.updates, eng.baseline)
+        st = eng.update_drafter(c["c_kl"], c["c_ce"], c["c_pg"], c["c_ent"], c["tau"], eng.baseline, lr=1e-3)
+        if st["fresh"] > 0:
+            eng.baseline = sched.ema(eng.baseline, st["fresh_accepted"] / st["fresh"])
+        eng.updates += 1
+        if stats is not None:
+            stats["update_ms"].append(eng.timings()["update"])
+            stats["update_rows"].append(st["rows"])
+
     def step(kk, stats=None, update=True, forced=None):
         lens_before = eng_lens[:]
         eng.draft(kk, forced=forced)
@@ -153,14 +165,7 @@ def main():
             eng_lens[b] += int(n[b])
         state["step"] += 1
         if update and wl.update_every and kk > 1 and state["step"] % wl.update_every == 0:
-            c = sched.coeffs(eng.updates, eng.baseline)
-            st = eng.update_drafter(c["c_kl"], c["c_ce"], c["c_pg"], c["c_ent"], c["tau"], eng.baseline, lr=1e-3)
-            if st["fresh"] > 0:
-                eng.baseline = sched.ema(eng.baseline, st["fresh_accepted"] / st["fresh"])
-            eng.updates += 1
-            if stats is not None:
-                stats["update_ms"].append(eng.timings()["update"])
-                stats["update_rows"].append(st["rows"])
+            update_drafter(stats)
         if stats is not None:
             tm = eng.timings()
             stats["tokens"] += int(n.sum())
@@ -266,6 +271,34 @@ def main():
         ar_tps = sa["tokens"] / (a1 - a0)
         ar = {"tokens_per_s": round(ar_tps, 2), "steps": KA, "speedup": round(value / ar_tps, 3)}
         log("plain AR on the same engine: %.1f tokens/s -> speedup %.2fx" % (ar_tps, value / ar_tps))
+    # The same decode loop through dvi_decode_steps: several steps per call, queued without a host
+    # synchronisation between them (the drafter update, where the workload trains, between calls).
+    dev = None
+    if not args.no_device_steps:
+        per_call = wl.update_every if (wl.update_every and k > 1) else 16
+        eng.prefill(prompts)
+        left = np.full(B, N - 1, np.int32)
+        _, n0, _ = eng.decode_steps(k, max(1, min(W, 64)), max_new=left)
+        left = left - n0.sum(axis=0)
+        calls = max(1, K // per_call)
+        dtok, dms = 0, []
+        torch.cuda.synchronize()
+        d0 = time.perf_counter()
+        for _ in range(calls):
+            _, n1, m1 = eng.decode_steps(k, per_call, max_new=left)
+            left = left - n1.sum(axis=0)
+            dtok += int(n1.sum())
+            dms.append(m1)
+            if wl.update_every and k > 1:
+                update_drafter()
+        torch.cuda.synchronize()
+        d1 = time.perf_counter()
+        dev_tps = dtok / (d1 - d0)
+        dev = {"tokens_per_s": round(dev_tps, 2), "steps": calls * per_call, "steps_per_call": per_call,
+               "ms_per_step": round(1e3 * (d1 - d0) / (calls * per_call), 4),
+               "mean_m": round(float(np.concatenate(dms).mean()), 4)}
+        log("dvi_decode_steps, %d steps per call: %.1f tokens/s, %.2f ms/step, mean m %.2f"
+            % (per_call, dev_tps, dev["ms_per_step"], dev["mean_m"]))
     # Full-acceptance ceiling: the same step with every draft forced to the verifier's own greedy
     # continuation (taken from a plain-decoding run), so each step commits k_spec tokens.  The
     # drafter head still runs in full (its argmax is replaced afterwards); no drafter updates.
@@ -346,6 +379,7 @@ def main():
                        "rate": round(float(mv.mean()) / k, 4)},
         "ar_baseline": ar,
         "full_acceptance": ceil,
+        "device_steps": dev,
         "prefill": prefill,
         "drafter_update": upd,
         "paper_context": PAPER_CONTEXT,
