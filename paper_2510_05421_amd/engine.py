@@ -174,9 +174,11 @@ class Engine:
         B, P = ids.shape
         lens = np.full(B, P, np.int32)
         first = np.empty(B, np.int32)
-        self._check(self.lib.dvi_prefill(self.ctx, B, ids.ctypes.data, lens.ctypes.data, P, first.ctypes.data))
-        self.batch = B
-        self.k_spec = 1   # read_logits() now returns the prefill head's row per sequence
+        st = self.lib.dvi_prefill(self.ctx, B, ids.ctypes.data, lens.ctypes.data, P, first.ctypes.data)
+        if st in (_abi.OK, _abi.ERR_NUMERIC):  # the prefill ran (a non-finite head logit is reported after it)
+            self.batch = B
+            self.k_spec = 1   # read_logits() now returns the prefill head's row per sequence
+        self._check(st)
         return first
 
     def draft(self, k_spec: int, forced=None, want: bool = False) -> Optional[np.ndarray]:

@@ -348,12 +348,25 @@ def test_state_capacity_and_numeric_errors():
         eng.draft(4, forced=np.array([[1, 2, 3, shape.vocab]]))
     assert e.value.status == ERR_ARG
     eng.draft(4)
+    with pytest.raises(DVIError) as e:   # several steps in one call need READY as well
+        eng.decode_steps(4, 1)
+    assert e.value.status == ERR_STATE
     eng.abort()                          # back to READY; lengths unchanged
     assert eng.lengths()[0] == 40
+    for bad_steps in (0, 65):
+        with pytest.raises(DVIError) as e:
+            eng.decode_steps(4, bad_steps)
+        assert e.value.status == ERR_ARG
+    with pytest.raises(DVIError) as e:   # checked up front: 40 + 2 steps x 4 + 4 > 48
+        eng.decode_steps(4, 3)
+    assert e.value.status == ERR_CAPACITY
+    assert eng.lengths()[0] == 40
+    tok, n, m = eng.decode_steps(4, 3, max_new=np.array([2], np.int32))  # 40 + 2 + 4 <= 48
+    assert int(n.sum()) == 2 and eng.lengths()[0] == 42
     eng.draft(4)
     eng.verify()
     tok, n, m = eng.commit()
-    L = 40 + int(n[0])
+    L = 42 + int(n[0])
     while L + 4 <= 48:
         eng.draft(4)
         eng.verify()
@@ -375,6 +388,12 @@ def test_state_capacity_and_numeric_errors():
     with pytest.raises(DVIError) as e:
         eng.commit()
     assert e.value.status == ERR_NUMERIC
+    eng.abort()
+    with pytest.raises(DVIError) as e:   # several steps: nothing committed from the bad step on
+        eng.decode_steps(2, 3)
+    assert e.value.status == ERR_NUMERIC
+    assert eng.lengths()[0] == 8
+    eng.draft(2)                         # the context is READY again
     eng.abort()
     eng.close()
 
