@@ -63,6 +63,9 @@ template <DType T, int MG, int EPI, int RT, int WMAX>
 __global__ void __launch_bounds__(64 * WMAX) gemm_kernel(GemmArgs a) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
     const int nt0 = blockIdx.x * RT;
+    // the last workgroup may hold fewer than RT tiles: tiles past N / 16 load nothing and store
+    // nothing (their MFMAs run on zeros)
+    const int nvalid = RT == 1 ? 1 : min(RT, a.N / 16 - nt0);
     const int KC = (T == DType::BF16) ? 32 : 16;
     const int KT = a.K / KC;
     const int c0 = (wave * KT) / nw, c1 = ((wave + 1) * KT) / nw;
@@ -99,7 +102,7 @@ __global__ void __launch_bounds__(64 * WMAX) gemm_kernel(GemmArgs a) {
         for (int k = 0; k < SSP; ++k) ssv[k] = src[min(lane + 64 * k, nparts - 1)];
     }
     EpiOperands<MG> pre;
-    if (kEarly && wave < RT) epilogue_prefetch<MG, EPI>(a, nt0 + wave, pre);
+    if (kEarly && wave < nvalid) epilogue_prefetch<MG, EPI>(a, nt0 + wave, pre);
 
     // Each activation fragment feeds RT weight tiles.  Loads go through a ring of S stages,
     // stage st holding chunk c + st: once a stage's MFMAs have issued it is refilled with the
@@ -112,13 +115,13 @@ __global__ void __launch_bounds__(64 * WMAX) gemm_kernel(GemmArgs a) {
         const bool in = cb < c1;
         const uint4 zero = {0u, 0u, 0u, 0u};
 #pragma unroll
-        for (int t = 0; t < RT; ++t) wf[t] = in ? ld_stream(wp + t * tile_stride + (size_t)cb * 64) : zero;
+        for (int t = 0; t < RT; ++t) wf[t] = (in && t < nvalid) ? ld_stream(wp + t * tile_stride + (size_t)cb * 64) : zero;
 #pragma unroll
         for (int g = 0; g < MG; ++g) xf[g] = (in && xv[g]) ? ld_stream(xp[g] + (size_t)cb * 64) : zero;
     };
 #pragma unroll
     for (int st = 0; st < S; ++st) fetch(c0 + st, w[st], x[st]);
-    if (kEarly && wave < RT) epilogue_prefetch_rope<MG, EPI>(a, nt0 + wave, pre);
+    if (kEarly && wave < nvalid) epilogue_prefetch_rope<MG, EPI>(a, nt0 + wave, pre);
     for (int c = c0; c < c1; c += S) {
 #pragma unroll
         for (int st = 0; st < S; ++st) {
@@ -155,7 +158,7 @@ __global__ void __launch_bounds__(64 * WMAX) gemm_kernel(GemmArgs a) {
         }
         __syncthreads();
     }
-    if (wave >= RT) return;
+    if (wave >= nvalid) return;
     const int nt = nt0 + wave;
 
     if (!kEarly) {
@@ -285,10 +288,11 @@ static GemmShape gemm_shape(int N, int K, int KC, int M) {
         while (rt > w) rt >>= 1;
         // Workgroups this wide hold one compute unit's share of registers per 8 waves, so the
         // grid runs in rounds of (CUs x 8 / w) workgroups: take 3 tiles instead of 4 when that
-        // needs fewer tile-rounds (QKV at 7B: 256 workgroups, one full round, instead of 192).
-        if (rt == 4 && tiles % 3 == 0) {
+        // needs fewer tile-rounds (the last workgroup may hold fewer).  QKV at 7B: 256
+        // workgroups, one full round, instead of 192; gate/up: 2 rounds of 3 instead of 4.
+        if (rt == 4) {
             const long slots = (long)compute_units() * 8 / w;
-            auto cost = [&](int r) { return ((tiles / r + slots - 1) / slots) * r; };
+            auto cost = [&](int r) { return (((tiles + r - 1) / r + slots - 1) / slots) * r; };
             if (cost(3) < cost(4)) rt = 3;
         }
     }
@@ -328,7 +332,7 @@ static void gemm_dispatch_epi(Epi e, const GemmArgs &a, dim3 grid, dim3 block, h
 
 template <DType T>
 static void gemm_dispatch(Epi e, const GemmArgs &a, GemmShape sh, hipStream_t s, const LaunchEvents &ev) {
-    dim3 grid(a.N / 16 / sh.rt), block(64 * sh.waves);
+    dim3 grid((a.N / 16 + sh.rt - 1) / sh.rt), block(64 * sh.waves);
     if (sh.waves > 8) {
         gemm_dispatch_epi<T, 1, 16>(e, a, grid, block, s, ev);
         return;
