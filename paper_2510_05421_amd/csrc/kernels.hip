@@ -69,6 +69,12 @@ __global__ void __launch_bounds__(64 * WMAX) gemm_kernel(GemmArgs a) {
     const int KC = (T == DType::BF16) ? 32 : 16;
     const int KT = a.K / KC;
     const int c0 = (wave * KT) / nw, c1 = ((wave + 1) * KT) / nw;
+    // A wave takes its chunks in a rotated order, c0 + rot .. c1 - 1 then c0 .. c0 + rot - 1.
+    // Without it every workgroup streams the same offset of its tile at the same time, and that
+    // lockstep costs bandwidth (down projection at one row: 19.5 -> 17.5 us).  rot depends only
+    // on the 12-tile group of the tile (one group holds whole workgroups of 1, 2, 3 or 4 tiles),
+    // so a tile's chunk order, and its rounding, is the same at every M.
+    const int rot = (nt0 / 12) % (c1 - c0);
     const size_t es = (T == DType::BF16) ? 2 : 4;
     const uint4 *wp = (const uint4 *)a.W + (size_t)nt0 * KT * 64 + lane;
     const size_t tile_stride = (size_t)KT * 64;
@@ -108,16 +114,17 @@ __global__ void __launch_bounds__(64 * WMAX) gemm_kernel(GemmArgs a) {
     // stage st holding chunk c + st: once a stage's MFMAs have issued it is refilled with the
     // chunk S ahead, so S - 1 chunks are always in flight while one is multiplied (the same
     // registers as double-buffering S/2 chunks, with more of them in flight).  Chunks are
-    // accumulated in order c0, c0 + 1, ..., c1 - 1 whatever S is.
+    // accumulated in the wave's rotated order whatever S is.
     constexpr int S = 4;
     uint4 w[S][RT], x[S][MG];
     auto fetch = [&](int cb, uint4 (&wf)[RT], uint4 (&xf)[MG]) {
         const bool in = cb < c1;
+        const int cr = cb + rot - (cb + rot >= c1 ? c1 - c0 : 0);  // the chunk step cb - c0 reads
         const uint4 zero = {0u, 0u, 0u, 0u};
 #pragma unroll
-        for (int t = 0; t < RT; ++t) wf[t] = (in && t < nvalid) ? ld_stream(wp + t * tile_stride + (size_t)cb * 64) : zero;
+        for (int t = 0; t < RT; ++t) wf[t] = (in && t < nvalid) ? ld_stream(wp + t * tile_stride + (size_t)cr * 64) : zero;
 #pragma unroll
-        for (int g = 0; g < MG; ++g) xf[g] = (in && xv[g]) ? ld_stream(xp[g] + (size_t)cb * 64) : zero;
+        for (int g = 0; g < MG; ++g) xf[g] = (in && xv[g]) ? ld_stream(xp[g] + (size_t)cr * 64) : zero;
     };
 #pragma unroll
     for (int st = 0; st < S; ++st) fetch(c0 + st, w[st], x[st]);
