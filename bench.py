@@ -38,13 +38,23 @@ KERNEL_NAMES = {"gate_up": "gemm_kernel<bf16,MG=1,EPI_SWIGLU> (gate/up projectio
 # (FETCH_SIZE, WRITE_SIZE) over this benchmark, scaled by what the same counters read for a
 # plain device copy.  Used only while the kernel source it was taken on is unchanged.
 TRAFFIC_PROFILES = {"gate_up": "profiles/gemm_gate_up_7b_b1_k4_traffic.md"}
-KERNEL_SOURCE = "paper_2510_05421_amd/csrc/kernels.hip"
+# the device code of every kernel: a counter summary stands only while these are unchanged
+KERNEL_SOURCES = ("paper_2510_05421_amd/csrc/kernels.hip", "paper_2510_05421_amd/csrc/device.h")
+
+
+def kernel_sources_sha256():
+    """SHA-256 over the kernel sources, in the order listed."""
+    import hashlib
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
 
 
 def measured_traffic(probe, workload, k_spec):
     """Bytes per launch from the committed counter summary, or None when there is none for
     this kernel and workload or the kernel source has changed since it was taken."""
-    import hashlib
     rel = TRAFFIC_PROFILES.get(probe)
     if rel is None or not os.path.exists(os.path.join(ROOT, rel)):
         return None
@@ -54,9 +64,7 @@ def measured_traffic(probe, workload, k_spec):
             if line.startswith("- `") and "`: " in line:
                 key, val = line[3:].split("`: ", 1)
                 fields[key] = val.strip().strip("`")
-    with open(os.path.join(ROOT, KERNEL_SOURCE), "rb") as f:
-        sha = hashlib.sha256(f.read()).hexdigest()
-    if (fields.get("kernels_hip_sha256") != sha or fields.get("workload") != workload
+    if (fields.get("kernel_sources_sha256") != kernel_sources_sha256() or fields.get("workload") != workload
             or fields.get("k_spec") != str(k_spec)):
         return None
     return int(float(fields["traffic_bytes_per_launch"]))

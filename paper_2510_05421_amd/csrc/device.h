@@ -215,7 +215,18 @@ struct EpiOperands {
     float v[MG][4];  // RESID: H row values; QKV: (cos, sin) of the lane's two rotary pairs
     float g[4];      // RESID: g_next
     int pos[MG];     // QKV: position of the token
+    float4 la;       // LOGITS with LoRA: float4 `lane` of the tile's A_s block (16 rows x r)
 };
+
+// The LoRA term of the logits epilogue takes A_s from registers when the rank is a multiple of
+// 4 up to 16: the tile's 16 x r block is requested with the other epilogue operands, one float4
+// per lane, and handed to the lanes that need it by shuffles; u (written by the kernel before)
+// is read in the epilogue, all ranks at once.  Other ranks read both in the epilogue.
+__device__ __forceinline__ bool lora_in_regs(const GemmArgs &a) { return a.r <= 16 && a.r % 4 == 0; }
+
+__device__ __forceinline__ float f4_get(const float4 &v, int k) {
+    return k == 0 ? v.x : k == 1 ? v.y : k == 2 ? v.z : v.w;
+}
 
 // Stage 1: everything but the rotary table, whose address needs the position.  m0: token of
 // the first row group.
@@ -244,6 +255,11 @@ __device__ __forceinline__ void epilogue_prefetch(const GemmArgs &a, int nt, Epi
         e.g[1] = g4.y;
         e.g[2] = g4.z;
         e.g[3] = g4.w;
+    }
+    if (EPI == EPI_LOGITS && a.lora_A != nullptr && lora_in_regs(a)) {
+        // the block is 16 r floats = 4 r float4s, 256-byte aligned (r % 4 == 0)
+        e.la = lane < 4 * a.r ? *(const float4 *)(a.lora_A + (size_t)nt * 16 * a.r + 4 * lane)
+                              : make_float4(0.f, 0.f, 0.f, 0.f);
     }
 }
 
@@ -359,11 +375,26 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &a, int nt, const f
                     gn[j] = -logf(-logf(u));
                 }
             }
+            const bool lregs = a.lora_A != nullptr && lora_in_regs(a);
+            float uv[16];
+            if (lregs)
+#pragma unroll
+                for (int cc = 0; cc < 16; ++cc)
+                    uv[cc] = (cc < a.r && valid) ? a.lora_u[(size_t)m * a.r + cc] : 0.f;
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const int n = nt * 16 + 4 * G4 + j;
                 float y = v[j] * sc;
-                if (a.lora_A != nullptr && valid) {
+                if (lregs) {
+                    // A_s[n][cc] is component cc % 4 of float4 (row * r + cc) / 4 of the block,
+                    // held by that lane; the sum runs over cc in order, as below
+                    const int row = 4 * G4 + j;
+                    float sacc = 0.f;
+#pragma unroll
+                    for (int cc = 0; cc < 16; ++cc)
+                        if (cc < a.r) sacc += __shfl(f4_get(e.la, cc & 3), (row * a.r + cc) >> 2) * uv[cc];
+                    if (valid) y = y + a.gamma * sacc;
+                } else if (a.lora_A != nullptr && valid) {
                     const float *Ar = a.lora_A + (size_t)n * a.r;
                     const float *ur = a.lora_u + (size_t)m * a.r;
                     float sacc = 0.f;

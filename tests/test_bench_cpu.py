@@ -60,3 +60,11 @@ def test_more_than_one_gpu_is_refused():
     assert r.returncode != 0
     assert "one GPU" in r.stderr
     assert r.stdout == ""
+
+
+def test_traffic_profile_is_used_only_for_its_sources_and_workload():
+    # the committed counter summary carries the SHA-256 of the kernel sources it was taken with
+    got = bench.measured_traffic("gate_up", "7b", 4)
+    assert isinstance(got, int) and 170_000_000 < got < 200_000_000  # about the 180.4 MB of weights
+    assert bench.measured_traffic("gate_up", "7b", 6) is None
+    assert bench.measured_traffic("gate_up", "13b", 4) is None
