@@ -643,3 +643,35 @@ def test_edge_shapes_are_lossless(B, P, k):
     _say("edge B=%d P=%d k_spec=%d: %d steps, mean m %.2f, %d/%d tokens agree with the oracle"
          % (B, P, k, info["steps"], info["m"].mean(), agree, T))
     eng.close()
+
+
+@pytest.mark.parametrize("name,r", [("tiny", 4), ("tiny", 6), ("tiny", 24), ("tiny", 64), ("1b_L4", 8),
+                                    ("1b_L4", 20)])
+def test_draft_head_logits_at_other_lora_ranks(name, r):
+    """The draft head's logits W^V h + gamma A_s (B_s h) against the oracle at LoRA ranks other
+    than the workloads' 16: multiples of 4 up to 16 take the epilogue's register path, the others
+    read A_s and u from memory.  The position checked is the second draft, whose input token is
+    forced, so both sides run the same sequence."""
+    shape = gu.SHAPES[name].replace(lora_rank=r)
+    w = synth.make_weights(shape, 0, lora_A_std=0.05)
+    P = 12
+    prompt = synth.make_prompts(shape.vocab, 1, P, 3)[0]
+    _say("draft head %s lora_rank=%d" % (name, r))
+    eng, _ = gu.engine(shape, max_seq=P + 8, weights=w)
+    first = int(eng.prefill(prompt[None])[0])
+    f0 = (first * 7 + 3) % shape.vocab
+    eng.draft(2, forced=np.array([[f0, 1]], np.int32))
+    got = eng.read_draft_logits()[0]
+    eng.close()
+    om = oracle.OracleModel(w)
+    cache = om.new_cache(P + 4)
+    om.layers(cache, om.embed(prompt), 0, 0, shape.n_layers)
+    om.layers(cache, om.embed([first]), P, 0, shape.split_k)
+    hn = om.final_norm(om.layers(cache, om.embed([f0]), P + 1, 0, shape.split_k))
+    A, B = w.lora_A.astype(np.float64), w.lora_B.astype(np.float64)
+    ref = om.draft_logits(hn, A, B, shape.lora_gamma)[0]
+    plain = om.draft_logits(hn, np.zeros_like(A), B, shape.lora_gamma)[0]
+    e = gu.rel_l2(got, ref)
+    _say("  relative L2 error %.3g (the LoRA term moves the logits by %.3g)" % (e, gu.rel_l2(plain, ref)))
+    assert gu.rel_l2(plain, ref) > 5 * gu.tol(shape)
+    assert e <= gu.tol(shape)
