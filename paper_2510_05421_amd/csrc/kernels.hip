@@ -71,9 +71,9 @@ __global__ void __launch_bounds__(64 * WMAX) gemm_kernel(GemmArgs a) {
     const int c0 = (wave * KT) / nw, c1 = ((wave + 1) * KT) / nw;
     // A wave takes its chunks in a rotated order, c0 + rot .. c1 - 1 then c0 .. c0 + rot - 1.
     // Without it every workgroup streams the same offset of its tile at the same time, and that
-    // lockstep costs bandwidth (down projection at one row: 19.5 -> 17.5 us).  rot depends only
-    // on the 12-tile group of the tile (one group holds whole workgroups of 1, 2, 3 or 4 tiles),
-    // so a tile's chunk order, and its rounding, is the same at every M.
+    // lockstep costs bandwidth (down projection at one row, measured alone: 19.5 -> 17.5 us).
+    // rot depends only on the 12-tile group of the tile (one group holds whole workgroups of 1,
+    // 2, 3 or 4 tiles), so a tile's chunk order, and its rounding, is the same at every M.
     const int rot = (nt0 / 12) % (c1 - c0);
     const size_t es = (T == DType::BF16) ? 2 : 4;
     const uint4 *wp = (const uint4 *)a.W + (size_t)nt0 * KT * 64 + lane;
