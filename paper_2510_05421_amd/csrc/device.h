@@ -337,15 +337,18 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &a, int nt, const f
                         float *q = a.Q + (size_t)m * a.n_heads * a.hd + hg * a.hd;
                         q[j] = x0;
                         q[j + half] = x1;
-                    } else if (hg < a.n_heads + a.n_kv) {  // key cache [b][kv][pos][hd]
-                        const size_t base = (((size_t)b * a.n_kv + (hg - a.n_heads)) * a.s_max + pos) * a.hd;
-                        St<T>::store(a.Kc, base + j, x0);
-                        St<T>::store(a.Kc, base + j + half, x1);
-                    } else {  // value cache, chunk-major: [b][kv][pos / 64][hd][pos % 64]
-                        const size_t base = ((size_t)b * a.n_kv + (hg - a.n_heads - a.n_kv)) * a.hd * a.s_max +
-                                            (size_t)(pos / CK) * a.hd * CK + pos % CK;
-                        St<T>::store(a.Vc, base + (size_t)j * CK, x0);
-                        St<T>::store(a.Vc, base + (size_t)(j + half) * CK, x1);
+                    } else {  // key or value cache: the position's 64-position block, fragment-major
+                        const bool key = hg < a.n_heads + a.n_kv;
+                        const int kvh = hg - a.n_heads - (key ? 0 : a.n_kv), kk = pos % CK;
+                        const int kc = (T == DType::BF16) ? 32 : 16;
+                        const size_t blk = (((size_t)b * a.n_kv + kvh) * a.s_max + (size_t)(pos - kk)) * a.hd;
+                        if (key) {
+                            St<T>::store(a.Kc, blk + kv_key_offset(kc, a.hd, kk, j), x0);
+                            St<T>::store(a.Kc, blk + kv_key_offset(kc, a.hd, kk, j + half), x1);
+                        } else {
+                            St<T>::store(a.Vc, blk + kv_val_offset(kc, a.hd, kk, j), x0);
+                            St<T>::store(a.Vc, blk + kv_val_offset(kc, a.hd, kk, j + half), x1);
+                        }
                     }
                 }
             }

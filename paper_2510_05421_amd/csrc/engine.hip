@@ -1107,28 +1107,29 @@ extern "C" dvi_status dvi_read_kv(dvi_ctx *x, int32_t layer, int32_t seq, int32_
     if (layer < 0 || layer >= cf.n_layers || seq < 0 || seq >= cf.max_batch || pos0 < 0 || npos < 0 ||
         pos0 + npos > cf.max_seq)
         return fail(x, DVI_ERR_ARG, "read_kv range");
-    const size_t es = x->es, hd = cf.head_dim, row = hd * es, cap = x->s_cap;
+    const size_t es = x->es, hd = cf.head_dim, cap = x->s_cap;
     if (npos == 0) return DVI_OK;
-    // values are stored chunk-major ([pos / 64][hd][pos % 64]); fetch the whole chunks that
-    // cover the range, then gather
-    const int c0 = pos0 / 64, nc = (pos0 + npos - 1) / 64 - c0 + 1;
+    // both caches are stored in fragment-major blocks of 64 positions: fetch the whole blocks
+    // that cover the range, then gather [n_kv][npos][hd]
+    const int c0 = pos0 / 64, nc = (pos0 + npos - 1) / 64 - c0 + 1, kc = pack_kc(x->dt);
     const size_t cbytes = hd * 64 * es;
-    std::vector<uint8_t> vt((size_t)cf.n_kv_heads * nc * cbytes);
+    std::vector<uint8_t> kt((size_t)cf.n_kv_heads * nc * cbytes), vt(kt.size());
     for (int h = 0; h < cf.n_kv_heads; ++h) {
-        const size_t off = (((size_t)seq * cf.n_kv_heads + h) * cap + pos0) * row;
-        HIPCHK(x, hipMemcpyAsync((uint8_t *)k + (size_t)h * npos * row, (uint8_t *)x->L[layer].Kc + off, npos * row,
+        const size_t off = (((size_t)seq * cf.n_kv_heads + h) * cap + (size_t)c0 * 64) * hd * es;
+        HIPCHK(x, hipMemcpyAsync(kt.data() + (size_t)h * nc * cbytes, (uint8_t *)x->L[layer].Kc + off, nc * cbytes,
                                  hipMemcpyDeviceToHost, x->stream));
-        const size_t voff = ((size_t)seq * cf.n_kv_heads + h) * hd * cap * es + (size_t)c0 * cbytes;
-        HIPCHK(x, hipMemcpyAsync(vt.data() + (size_t)h * nc * cbytes, (uint8_t *)x->L[layer].Vc + voff, nc * cbytes,
+        HIPCHK(x, hipMemcpyAsync(vt.data() + (size_t)h * nc * cbytes, (uint8_t *)x->L[layer].Vc + off, nc * cbytes,
                                  hipMemcpyDeviceToHost, x->stream));
     }
     HIPCHK(x, hipStreamSynchronize(x->stream));
     for (int h = 0; h < cf.n_kv_heads; ++h)
         for (int p = 0; p < npos; ++p) {
             const int pa = pos0 + p, c = pa / 64 - c0, o = pa % 64;
-            for (size_t d = 0; d < hd; ++d)
-                memcpy((uint8_t *)v + (((size_t)h * npos + p) * hd + d) * es,
-                       vt.data() + (((size_t)h * nc + c) * hd + d) * 64 * es + (size_t)o * es, es);
+            const size_t blk = ((size_t)h * nc + c) * cbytes, dst = ((size_t)h * npos + p) * hd * es;
+            for (int d = 0; d < (int)hd; ++d) {
+                memcpy((uint8_t *)k + dst + d * es, kt.data() + blk + kv_key_offset(kc, (int)hd, o, d) * es, es);
+                memcpy((uint8_t *)v + dst + d * es, vt.data() + blk + kv_val_offset(kc, (int)hd, o, d) * es, es);
+            }
         }
     return DVI_OK;
 }

@@ -18,6 +18,27 @@ inline size_t dtype_size(DType t) { return t == DType::BF16 ? 2 : 4; }
 // 16 bytes are directly its MFMA A-operand fragment.
 inline int pack_kc(DType t) { return t == DType::BF16 ? 32 : 16; }
 
+// KV cache layout.  Both caches hold, per (sequence, kv head), blocks of 64 positions, block c
+// at element offset (c * 64) * hd of the head's region [s_max * hd].  Inside a block the
+// elements are fragment-major like the weights: 1 KiB fragments whose 16 bytes per lane are an
+// MFMA operand of the attention as loaded.  KC and EPL as for the weights.
+//   keys   (B operand of S = Q K^T): fragment (kk / 16) * (hd / KC) + d / KC, lane
+//          kk % 16 + 16 * ((d % KC) / EPL), element d % EPL;
+//   values (B operand of O = P V):   fragment (d / 16) * (64 / KC) + kk / KC, lane
+//          d % 16 + 16 * ((kk % KC) / EPL), element kk % EPL;
+// for position kk (0..63) of the block and head dim d.  The functions give the element offset
+// inside the block.
+__host__ __device__ inline size_t kv_key_offset(int kc, int hd, int kk, int d) {
+    const int epl = kc / 4;
+    const int f = (kk / 16) * (hd / kc) + d / kc, l = kk % 16 + 16 * ((d % kc) / epl);
+    return ((size_t)f * 64 + l) * epl + d % epl;
+}
+__host__ __device__ inline size_t kv_val_offset(int kc, int hd, int kk, int d) {
+    const int epl = kc / 4;
+    const int f = (d / 16) * (64 / kc) + kk / kc, l = d % 16 + 16 * ((kk % kc) / epl);
+    return ((size_t)f * 64 + l) * epl + kk % epl;
+}
+
 // Rows of a packed matrix may be permuted (see the epilogues): prow[i] = src * 2^24 + row
 // means packed row i is row `row` of source matrix `src` (up to three sources).
 struct PackSrc {
@@ -55,8 +76,8 @@ struct GemmArgs {
     const float *g_next;
     // EPI_QKV
     float *Q;           // [M][n_heads * hd] fp32
-    void *Kc, *Vc;      // this layer's caches: keys [max_batch][n_kv][s_max][hd], values
-                        // chunk-major [max_batch][n_kv][s_max / 64][hd][64]
+    void *Kc, *Vc;      // this layer's caches [max_batch][n_kv][s_max / 64][64-position block],
+                        // blocks fragment-major (kv_key_offset, kv_val_offset)
     int n_heads, n_kv, hd, s_max;
     const float2 *rope; // [s_max][hd/2] (cos, sin)
     // EPI_SWIGLU
@@ -112,8 +133,8 @@ constexpr int kMaxBatch = 64;
 
 struct AttnArgs {
     const float *Q;      // [M][n_heads*hd]
-    const void *Kc;      // [max_batch][n_kv][s_max][hd]
-    const void *Vc;      // [max_batch][n_kv][s_max / 64][hd][64] (chunk-major)
+    const void *Kc;      // [max_batch][n_kv][s_max / 64][block], blocks as kv_key_offset
+    const void *Vc;      // [max_batch][n_kv][s_max / 64][block], blocks as kv_val_offset
     const int32_t *lens; // [B] cache length of every sequence (device memory, so that a captured
                          // graph replays with the current lengths)
     int B, c, pos_off;

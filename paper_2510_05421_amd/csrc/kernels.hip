@@ -609,10 +609,11 @@ constexpr long kAttnLargeGrid = 2048;  // chunk-waves from which the merge takes
 // One wave's 64-key chunk ch of (sequence b, kv head kvh), nk of its keys in the cache.
 // Keys are cut into 64-position chunks at absolute positions; the query rows that read this kv
 // head (c tokens x n_heads/n_kv grouped heads) are taken 16 at a time as the MFMA row dimension:
-//   S = Q K^T      A = query fragments, B = key fragments read straight from the key cache;
+//   S = Q K^T      A = query fragments, B = key fragments read straight from the key cache's
+//                  fragment-major block of the chunk;
 //   softmax        per row over the chunk's 64 keys: max, p = exp(s - max), sum (fixed tree);
 //   O = P V        P goes through the wave's LDS tile Ps into A-operand layout; B = value
-//                  fragments read straight from the chunk-major value cache.
+//                  fragments read straight from the value cache's block.
 // Row at position p sees keys 0..p (block-causal); keys past a row's position, or past the
 // cached length, are masked before the max and multiply as zeros.  Each row's unnormalised
 // output, max and sum go to sink(row, head dim, value, with_stats, max, sum).  Rows are
@@ -651,27 +652,28 @@ struct AttnTile {
     // Every position of a 64-key chunk lies inside the cache row (the row length is a multiple of
     // 64), so the fragment loads are unconditional.  Keys at or past nk (not yet written, or past
     // the block) get score -inf, whatever they hold, so key fragments need no mask.
-    // Key fragments: tile t holds keys 16t + l16; head dims step*KC + EPL*lg .. +EPL.
+    // Key fragments: tile t holds keys 16t + l16; head dims step*KC + EPL*lg .. +EPL.  The
+    // cache block is fragment-major (kv_key_offset), so fragment (t, step) is 1 KiB at
+    // (t * DS + step) KiB and each load is contiguous across the wave.
     static __device__ __forceinline__ void load_k(const AttnArgs &a, int b, int kvh, int ch, KFrag &kf) {
-        const int lane = threadIdx.x & 63, l16 = lane & 15, lg = lane >> 4;
-        const size_t kc0 = ((size_t)b * a.n_kv + kvh) * a.s_max + (size_t)ch * CK;
+        const int lane = threadIdx.x & 63;
+        const uint4 *blk =
+            (const uint4 *)((const E *)a.Kc + (((size_t)b * a.n_kv + kvh) * a.s_max + (size_t)ch * CK) * HD) + lane;
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
-            const uint4 *src = (const uint4 *)((const E *)a.Kc + (kc0 + 16 * t + l16) * HD + EPL * lg);
+        for (int t = 0; t < 4; ++t)
 #pragma unroll
-            for (int st = 0; st < DS; ++st) kf[t][st] = src[st * (KC * sizeof(E) / 16)];
-        }
+            for (int st = 0; st < DS; ++st) kf[t][st] = blk[(t * DS + st) * 64];
     }
-    // Value fragments: tile dt holds head dim 16 dt + l16; keys step*KC + EPL*lg .. +EPL.
+    // Value fragments: tile dt holds head dim 16 dt + l16; keys step*KC + EPL*lg .. +EPL, at
+    // fragment dt * KS + step of the block (kv_val_offset).
     static __device__ __forceinline__ void load_v(const AttnArgs &a, int b, int kvh, int ch, VFrag &vf) {
-        const int lane = threadIdx.x & 63, l16 = lane & 15, lg = lane >> 4;
-        const size_t vt0 = ((size_t)b * a.n_kv + kvh) * HD * a.s_max + (size_t)ch * HD * CK;
+        const int lane = threadIdx.x & 63;
+        const uint4 *blk =
+            (const uint4 *)((const E *)a.Vc + (((size_t)b * a.n_kv + kvh) * a.s_max + (size_t)ch * CK) * HD) + lane;
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) {
-            const E *src = (const E *)a.Vc + vt0 + (16 * dt + l16) * CK + EPL * lg;
+        for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) vf[dt][ks] = *(const uint4 *)(src + ks * KC);
-        }
+            for (int ks = 0; ks < KS; ++ks) vf[dt][ks] = blk[(dt * KS + ks) * 64];
     }
     static __device__ __forceinline__ void pack_q(const QRaw &qraw, int r0, int R, uint4 (&qf)[DS]) {
         const bool ok = r0 + ((threadIdx.x & 63) & 15) < R;
