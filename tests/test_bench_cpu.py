@@ -62,9 +62,23 @@ def test_more_than_one_gpu_is_refused():
     assert r.stdout == ""
 
 
-def test_traffic_profile_is_used_only_for_its_sources_and_workload():
-    # the committed counter summary carries the SHA-256 of the kernel sources it was taken with
-    got = bench.measured_traffic("gate_up", "7b", 4)
-    assert isinstance(got, int) and 170_000_000 < got < 200_000_000  # about the 180.4 MB of weights
+def test_traffic_profile_is_used_only_for_its_sources_and_workload(tmp_path, monkeypatch):
+    # a counter summary names the kernel sources' SHA-256, the workload and k_spec it was taken
+    # with; bench.py takes its traffic figure only when all three match
+    prof = tmp_path / "traffic.md"
+    prof.write_text("- `kernel_sources_sha256`: `abc`\n- `workload`: `7b`\n- `k_spec`: `4`\n"
+                    "- `traffic_bytes_per_launch`: `181040071`\n")
+    monkeypatch.setattr(bench, "TRAFFIC_PROFILES", {"gate_up": str(prof)})
+    monkeypatch.setattr(bench, "kernel_sources_sha256", lambda: "abc")
+    assert bench.measured_traffic("gate_up", "7b", 4) == 181040071
     assert bench.measured_traffic("gate_up", "7b", 6) is None
     assert bench.measured_traffic("gate_up", "13b", 4) is None
+    assert bench.measured_traffic("qkv", "7b", 4) is None
+    monkeypatch.setattr(bench, "kernel_sources_sha256", lambda: "def")
+    assert bench.measured_traffic("gate_up", "7b", 4) is None
+
+
+def test_kernel_sources_hash_covers_both_device_files():
+    assert len(bench.KERNEL_SOURCES) == 2
+    assert all(os.path.exists(os.path.join(ROOT, f)) for f in bench.KERNEL_SOURCES)
+    assert len(bench.kernel_sources_sha256()) == 64
