@@ -675,3 +675,35 @@ def test_draft_head_logits_at_other_lora_ranks(name, r):
     _say("  relative L2 error %.3g (the LoRA term moves the logits by %.3g)" % (e, gu.rel_l2(plain, ref)))
     assert gu.rel_l2(plain, ref) > 5 * gu.tol(shape)
     assert e <= gu.tol(shape)
+
+
+@pytest.mark.parametrize("name,P", [("tiny", 70), ("1b_L4", 66), ("7b_L4", 66)])
+def test_cache_keys_and_values_match_the_oracle(name, P):
+    """The cache's keys (after the rotary embedding) and values at every committed position,
+    read back through the ABI, equal the oracle's cache for the same tokens within the storage
+    tolerance.  The prompt crosses a 64-position block boundary, and decoding writes on both
+    sides of it."""
+    shape = gu.SHAPES[name]
+    T = 8
+    w = synth.make_weights(shape, 0, lora_A_std=0.05)
+    prompt = synth.make_prompts(shape.vocab, 1, P, 17)[0]
+    eng, _ = gu.engine(shape, max_seq=P + T + 8, weights=w)
+    toks, _ = eng.generate(prompt[None], T, KSPEC[name])
+    n = int(eng.lengths()[0])            # positions whose keys/values are committed
+    assert n == P + T - 1
+    got = [eng.read_kv(l, 0, 0, n) for l in range(shape.n_layers)]
+    eng.close()
+    seq = np.concatenate([prompt, toks[0]])[:n]
+    om = oracle.OracleModel(w)
+    cache = om.new_cache(n)
+    om.layers(cache, om.embed(seq), 0, 0, shape.n_layers)
+    worst = 0.0
+    for l, (k, v) in enumerate(got):
+        # oracle [n, n_kv * hd] -> [n_kv, n, hd], the ABI's order
+        ko = cache[0][l].reshape(n, shape.n_kv_heads, shape.head_dim).transpose(1, 0, 2)
+        vo = cache[1][l].reshape(n, shape.n_kv_heads, shape.head_dim).transpose(1, 0, 2)
+        for got_x, ref_x in ((k, ko), (v, vo)):
+            e = gu.rel_l2(synth.bf16_bits_to_f32(got_x) if got_x.dtype == np.uint16 else got_x, ref_x)
+            worst = max(worst, e)
+            assert e <= gu.tol(shape), "layer %d: relative L2 error %.3g" % (l, e)
+    _say("cache %s P=%d: %d positions, worst relative L2 error %.3g" % (name, P, n, worst))
