@@ -21,12 +21,17 @@ What pins each part (tests/test_oracle_pins.py, tests/test_oracle_update_pins.py
                       complex-number rotary embedding; GQA == MHA with shared kv
                       weights; block == token-by-token (bitwise); scipy softmax for
                       one attention row; A_s = 0 draft head == target head
-  greedy_ar           the definition itself (argmax of the pinned forward)
+  greedy_ar           the definition itself (argmax of the pinned forward); the gap it
+                      records per token is its logits row's top-2 gap
+  top2_gap            hand values (a tie for the maximum gives 0), a sorted-values brute
+                      force on batched rows with repeats and on 32000-wide rows
   dvi_generate        losslessness (== greedy_ar for random LoRA, forced-wrong and
                       forced-right drafts, k_spec 1/2/4/8); every m forced by
                       construction; brute-force m; split k = L accepts everything;
                       buffer count / reward pattern; rolled-back cache bitwise equal
-                      across different rejected drafts and to the AR cache
+                      across different rejected drafts and to the AR cache; each logged
+                      row's prev_id is the token whose state drafted it, and its h_hat is
+                      reproduced bitwise by a fresh forward ending in that token
   loss_and_grad       finite differences per term; scipy rel_entr / entropy for the
                       loss terms; closed-form dL/dz for masked CE; row sums of
                       dL/dz = 0; KL = 0 and gradient 0 at z = logits/tau; A_s = 0 =>

@@ -52,41 +52,135 @@ static inline double wget(const void *w, int bf16, size_t i) {
 
 /*
  * Y[t][j] = sum_{c=0}^{K-1} W[j][c] * X[t][c]   (W row-major [N][K]),
- * the sum taken in increasing c.  Rows of W are visited in groups of four and
- * tokens in groups of TB only to keep the CPU busy; each Y[t][j] still sees
- * exactly the same sequence of multiplies and adds.
+ * each sum taken in increasing c, one multiply and one add per term (no
+ * fused multiply-add: built with -ffp-contract=off).  Rows of W are widened
+ * to double RB at a time and tokens are taken TB at a time only to keep the
+ * CPU busy: the TB sums of a row are independent, so they may share SIMD
+ * lanes, and every Y[t][j] still sees exactly the same sequence of
+ * multiplies and adds.  The result therefore does not depend on the block
+ * sizes, the thread count, the SIMD width or how many tokens are processed
+ * together.  An AVX2 body is used where the CPU has it; the plain body
+ * evaluates the same operations in the same order.
  */
-#define TB 8
+#include <immintrin.h>
+#define TB 8      /* tokens per SIMD block (two 4-wide vectors) */
+#define TSUB 4    /* token blocks sharing one widened row panel */
+#define RB 4      /* rows per panel */
+#define RV 8      /* rows per panel of the one-token product */
+
+/* dst[c] = W[row][c] as double, c < K */
+__attribute__((target("avx2")))
+static void widen_row_avx2(const void *W, int bf16, size_t row, int K, double *dst) {
+    int c = 0;
+    if (bf16) {
+        const uint16_t *src = (const uint16_t *)W + row * K;
+        for (; c + 8 <= K; c += 8) {
+            const __m256i w = _mm256_slli_epi32(_mm256_cvtepu16_epi32(_mm_loadu_si128((const __m128i *)(src + c))), 16);
+            const __m256 f = _mm256_castsi256_ps(w);
+            _mm256_storeu_pd(dst + c, _mm256_cvtps_pd(_mm256_castps256_ps128(f)));
+            _mm256_storeu_pd(dst + c + 4, _mm256_cvtps_pd(_mm256_extractf128_ps(f, 1)));
+        }
+    } else {
+        const float *src = (const float *)W + row * K;
+        for (; c + 4 <= K; c += 4) _mm256_storeu_pd(dst + c, _mm256_cvtps_pd(_mm_loadu_ps(src + c)));
+    }
+    for (; c < K; ++c) dst[c] = wget(W, bf16, row * K + c);
+}
+
+static void widen_row_plain(const void *W, int bf16, size_t row, int K, double *dst) {
+    for (int c = 0; c < K; ++c) dst[c] = wget(W, bf16, row * K + c);
+}
+
+/* acc[jj][t] = sum_c P[jj][c] * XT[c*xs + t], jj < RB, t < TB; P is [RB][K] */
+__attribute__((target("avx2")))
+static void panel_avx2(const double *P, int K, const double *XT, int xs, double (*acc)[TB]) {
+    const double *p0 = P, *p1 = P + K, *p2 = P + 2 * (size_t)K, *p3 = P + 3 * (size_t)K;
+    __m256d a00 = _mm256_setzero_pd(), a01 = _mm256_setzero_pd(), a10 = _mm256_setzero_pd(), a11 = _mm256_setzero_pd();
+    __m256d a20 = _mm256_setzero_pd(), a21 = _mm256_setzero_pd(), a30 = _mm256_setzero_pd(), a31 = _mm256_setzero_pd();
+    for (int c = 0; c < K; ++c) {
+        const __m256d x0 = _mm256_loadu_pd(XT + (size_t)c * xs), x1 = _mm256_loadu_pd(XT + (size_t)c * xs + 4);
+        __m256d w = _mm256_broadcast_sd(p0 + c);
+        a00 = _mm256_add_pd(a00, _mm256_mul_pd(w, x0));
+        a01 = _mm256_add_pd(a01, _mm256_mul_pd(w, x1));
+        w = _mm256_broadcast_sd(p1 + c);
+        a10 = _mm256_add_pd(a10, _mm256_mul_pd(w, x0));
+        a11 = _mm256_add_pd(a11, _mm256_mul_pd(w, x1));
+        w = _mm256_broadcast_sd(p2 + c);
+        a20 = _mm256_add_pd(a20, _mm256_mul_pd(w, x0));
+        a21 = _mm256_add_pd(a21, _mm256_mul_pd(w, x1));
+        w = _mm256_broadcast_sd(p3 + c);
+        a30 = _mm256_add_pd(a30, _mm256_mul_pd(w, x0));
+        a31 = _mm256_add_pd(a31, _mm256_mul_pd(w, x1));
+    }
+    _mm256_storeu_pd(acc[0], a00); _mm256_storeu_pd(acc[0] + 4, a01);
+    _mm256_storeu_pd(acc[1], a10); _mm256_storeu_pd(acc[1] + 4, a11);
+    _mm256_storeu_pd(acc[2], a20); _mm256_storeu_pd(acc[2] + 4, a21);
+    _mm256_storeu_pd(acc[3], a30); _mm256_storeu_pd(acc[3] + 4, a31);
+}
+
+static void panel_plain(const double *P, int K, const double *XT, int xs, double (*acc)[TB]) {
+    for (int jj = 0; jj < RB; ++jj)
+        for (int t = 0; t < TB; ++t) {
+            double s = 0.0;
+            for (int c = 0; c < K; ++c) s += P[(size_t)jj * K + c] * XT[(size_t)c * xs + t];
+            acc[jj][t] = s;
+        }
+}
+
 static void matmul(const void *W, int bf16, int N, int K, int n, const double *X, double *Y) {
-    for (int t0 = 0; t0 < n; t0 += TB) {
-        int nb = n - t0 < TB ? n - t0 : TB;
-        double *XT = (double *)calloc((size_t)K * TB, sizeof(double));
-        for (int c = 0; c < K; ++c)
-            for (int t = 0; t < nb; ++t) XT[(size_t)c * TB + t] = X[(size_t)(t0 + t) * K + c];
-#pragma omp parallel for schedule(static)
-        for (int j = 0; j < N; j += 4) {
-            int jn = N - j < 4 ? N - j : 4;
-            double acc[4][TB];
-            memset(acc, 0, sizeof(acc));
-            if (nb == 1) {
+    const int avx2 = __builtin_cpu_supports("avx2");
+    if (n == 1) {
+        /* one token: RV independent row sums, each in increasing c */
+#pragma omp parallel
+        {
+            double *P = (double *)malloc(sizeof(double) * (size_t)RV * K);
+#pragma omp for schedule(static)
+            for (int j = 0; j < N; j += RV) {
+                const int jn = N - j < RV ? N - j : RV;
+                for (int jj = 0; jj < jn; ++jj)
+                    (avx2 ? widen_row_avx2 : widen_row_plain)(W, bf16, (size_t)(j + jj), K, P + (size_t)jj * K);
+                double acc[RV] = {0.0};
                 for (int c = 0; c < K; ++c) {
-                    double x = XT[(size_t)c * TB];
-                    for (int jj = 0; jj < jn; ++jj) acc[jj][0] += wget(W, bf16, (size_t)(j + jj) * K + c) * x;
+                    const double xc = X[c];
+                    for (int jj = 0; jj < RV; ++jj)
+                        if (jj < jn) acc[jj] += P[(size_t)jj * K + c] * xc;
                 }
-            } else {
-                for (int c = 0; c < K; ++c) {
-                    const double *xt = XT + (size_t)c * TB;
-                    for (int jj = 0; jj < jn; ++jj) {
-                        double w = wget(W, bf16, (size_t)(j + jj) * K + c);
-                        for (int t = 0; t < TB; ++t) acc[jj][t] += w * xt[t];
-                    }
+                for (int jj = 0; jj < jn; ++jj) Y[j + jj] = acc[jj];
+            }
+            free(P);
+        }
+        return;
+    }
+    const int TBB = TB * TSUB;
+    double *XT = (double *)malloc(sizeof(double) * (size_t)K * TBB);
+    for (int t0 = 0; t0 < n; t0 += TBB) {
+        const int nb = n - t0 < TBB ? n - t0 : TBB;
+        /* X block transposed to [K][TBB]; lanes past the block are zero and never stored */
+        for (int c = 0; c < K; ++c)
+            for (int t = 0; t < TBB; ++t) XT[(size_t)c * TBB + t] = t < nb ? X[(size_t)(t0 + t) * K + c] : 0.0;
+#pragma omp parallel
+        {
+            double *P = (double *)calloc((size_t)RB * K, sizeof(double));
+#pragma omp for schedule(static)
+            for (int j = 0; j < N; j += RB) {
+                const int jn = N - j < RB ? N - j : RB;
+                for (int jj = 0; jj < RB; ++jj) {
+                    if (jj < jn)
+                        (avx2 ? widen_row_avx2 : widen_row_plain)(W, bf16, (size_t)(j + jj), K, P + (size_t)jj * K);
+                    else
+                        memset(P + (size_t)jj * K, 0, sizeof(double) * K);
+                }
+                for (int sb = 0; sb < TSUB && sb * TB < nb; ++sb) {
+                    double acc[RB][TB];
+                    (avx2 ? panel_avx2 : panel_plain)(P, K, XT + sb * TB, TBB, acc);
+                    for (int jj = 0; jj < jn; ++jj)
+                        for (int t = 0; t < TB && sb * TB + t < nb; ++t) Y[(size_t)(t0 + sb * TB + t) * N + j + jj] = acc[jj][t];
                 }
             }
-            for (int jj = 0; jj < jn; ++jj)
-                for (int t = 0; t < nb; ++t) Y[(size_t)(t0 + t) * N + j + jj] = acc[jj][t];
+            free(P);
         }
-        free(XT);
     }
+    free(XT);
 }
 
 /* y = x / sqrt(mean(x^2) + eps) * g */

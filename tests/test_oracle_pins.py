@@ -194,6 +194,88 @@ def test_argmax_ties_go_to_lowest_id():
         assert int(oracle.argmax_lowest(m2.target_logits(hn))[0]) == lower
 
 
+def _top2_brute(row):
+    """Largest minus second largest entry, by sorting the row's values (repeats kept)."""
+    v = sorted((float(x) for x in row), reverse=True)
+    return v[0] - v[1]
+
+
+def test_top2_gap_hand_values_and_ties():
+    # a distinct runner-up; a tie for the maximum gives 0; negatives; the maximum anywhere
+    z = np.array([[3.0, 1.0, 2.0, 0.5],
+                  [5.0, 1.0, 5.0, 4.0],
+                  [-1.0, -3.0, -2.0, -1.5],
+                  [0.0, 0.0, 0.0, 7.25],
+                  [2.0, 2.0, 2.0, 2.0]])
+    assert list(oracle.top2_gap(z)) == [1.0, 0.0, 0.5, 7.25, 0.0]
+
+
+def test_top2_gap_against_sorting_on_batched_rows():
+    """Random rows with repeated values, in a [2, 3, V] batch: every row's gap equals the
+    sorted-values reference, and the last axis is the one reduced."""
+    rng = np.random.default_rng(7)
+    z = rng.integers(-6, 7, size=(2, 3, 11)).astype(np.float64) * 0.25
+    g = oracle.top2_gap(z)
+    assert g.shape == (2, 3)
+    for i in range(2):
+        for j in range(3):
+            assert g[i, j] == _top2_brute(z[i, j])
+    # continuous values: the gap is the difference of the two largest
+    z = rng.normal(size=(50, 32000))
+    ref = np.array([_top2_brute(r) for r in z])
+    assert np.array_equal(oracle.top2_gap(z), ref)
+    assert np.all(oracle.top2_gap(z) >= 0)
+
+
+def test_gaps_of_greedy_ar_are_those_of_its_logits():
+    """greedy_ar records, for every emitted token, the top-2 gap of the logits row it came from;
+    the emitted token is that row's argmax."""
+    w, m = _model(seed=16)
+    prompt = synth.make_prompts(PIN.vocab, 1, 7, 16)[0]
+    ar = dvi.greedy_ar(m, prompt, 12, keep_logits=True)
+    for t in range(12):
+        assert ar.gaps[t] == _top2_brute(ar.logits[t])
+        assert ar.tokens[t] == int(np.argmax(ar.logits[t]))
+
+
+def test_buffer_prev_id_and_state_come_from_the_same_token():
+    """Each logged row holds prev_id = the token whose state drafted it: the pending (last
+    committed) token for i = 1, else the draft i-1.  Its h_hat is RMSNorm of h_k computed from
+    that token at its position, which a fresh forward over (prompt, committed tokens, earlier
+    drafts of the block) reproduces bitwise."""
+    k_spec = 4
+    w, m, prompt, ar = _ar_and_prompt(seed=17, N=30)
+    rng = np.random.default_rng(5)
+
+    def forced(step, pos, out):
+        nxt = ar.tokens[len(out):len(out) + k_spec]
+        if nxt.size < k_spec:
+            return None
+        d = nxt.copy()
+        j = int(rng.integers(0, k_spec + 1))   # first wrong draft at j (none if j = k_spec)
+        if j < k_spec:
+            d[j] = (d[j] + 1) % PIN.vocab
+        return d
+
+    r = dvi.dvi_generate(m, prompt, 30, k_spec, _drafter(w), forced_drafts=forced)
+    assert np.array_equal(r.tokens, ar.tokens)
+    P, k = prompt.size, PIN.split_k
+    idx, checked = 0, 0
+    for s in r.steps:
+        rows = r.buffer[idx:idx + min(s.m + 1, k_spec)]
+        idx += len(rows)
+        committed = ar.tokens[:s.pos - P + 1]          # tokens committed before this step
+        for b in rows:
+            want_prev = int(committed[-1]) if b.i == 1 else int(s.drafts[b.i - 2])
+            assert b.prev_id == want_prev
+            seq = np.concatenate([prompt, committed, s.drafts[:b.i - 1]]).astype(np.int32)
+            assert seq[-1] == b.prev_id and seq.size == s.pos + b.i
+            hk = m.layers(m.new_cache(seq.size), m.embed(seq), 0, 0, k)
+            assert np.array_equal(m.final_norm(hk[-1:])[0], b.h_hat)
+            checked += 1
+    assert checked >= 10 and {b.i for b in r.buffer} >= {1, 2}
+
+
 # ----------------------------------------------------------------------------- losslessness
 def _ar_and_prompt(seed=10, P=9, N=30, shape=PIN):
     w, m = _model(shape, seed=seed)
