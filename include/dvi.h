@@ -130,10 +130,13 @@ void dvi_destroy(dvi_ctx *ctx);
  * Prefill (Section 3.3: the shallow state is computed once from the prefix):
  * run all L layers over each sequence's prompt, fill the KV cache, and emit
  * each sequence's first token x_P = argmax p_phi(. | h_{L,P-1}).  ids: HOST
- * int32 [batch, stride]; lens: HOST int32 [batch], all equal in this version,
- * 1 <= lens[b] <= stride; first_tok: HOST int32 [batch] (out).  The first token
- * is committed and becomes each sequence's pending token.  Allowed in any
- * state except DRAFTED/VERIFIED; resets all sequences.  -> READY
+ * int32 [batch, stride], sequence b's prompt in ids[b*stride .. b*stride+lens[b]);
+ * lens: HOST int32 [batch], each 1 <= lens[b] <= stride and lens[b] + 1 <= max_seq
+ * (prompts may differ in length; DVI_ERR_ARG / DVI_ERR_CAPACITY otherwise);
+ * first_tok: HOST int32 [batch] (out).  The first token is committed and
+ * becomes each sequence's pending token, and sequence b's cache length is
+ * lens[b].  Allowed in any state except DRAFTED/VERIFIED; resets all
+ * sequences.  -> READY
  */
 dvi_status dvi_prefill(dvi_ctx *ctx, int32_t batch, const int32_t *ids, const int32_t *lens, int32_t stride,
                        int32_t *first_tok);

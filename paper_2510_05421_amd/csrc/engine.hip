@@ -46,6 +46,16 @@ struct Bump {
     }
 };
 
+// Per-call scratch of a decode pass: attention partials (chunk_stride slots per row and head)
+// and merge counters, and the vocabulary head's per-tile argmax partials.
+struct Scratch {
+    float *att_po = nullptr, *att_pml = nullptr;
+    int32_t *att_cnt = nullptr;
+    int chunk_stride = 0;
+    float *part_val = nullptr;
+    int32_t *part_idx = nullptr;
+};
+
 }  // namespace
 
 struct dvi_ctx {
@@ -63,12 +73,12 @@ struct dvi_ctx {
     // (ss) and dtype(h * g) for the next folded RMSNorm (hg); hk/hk_ss/hk_hg hold the k_spec
     // drafted rows of every sequence (row b*k_spec + j), which the verify then continues.
     // GEMM inputs (hg, act, attn_o, hk_hg, dfm, pfm, ufm) are in the fragment-major layout.
-    float *h, *ss, *q, *hk, *hk_ss, *vlogits, *dlogits, *part_val, *lora_u, *att_po, *att_pml;
+    float *h, *ss, *q, *hk, *hk_ss, *vlogits, *dlogits, *lora_u;
     float *sinv_rows;  // 1/rms per token for prefill-block GEMMs
-    int32_t *att_cnt;
-    int chunk_stride = 0;
+    int chunk_stride = 0;  // 64-key chunks of the longest sequence (max_seq), the attention grid's cap
     void *hg, *attn_o, *act, *hk_hg, *hk_hat, *dfm, *pfm, *ufm;
-    int32_t *part_idx;
+    // scratch in the workspace (ws_scr), and the scratch the launches use (scr)
+    Scratch ws_scr, scr;
     // small device state; io block is one contiguous region copied back at commit
     int32_t *lens, *pending, *drafts, *targets, *forced, *max_new, *ids, *copy_list, *ring_state;
     int32_t *rng_step;  // [0]: decode steps committed since the prefill (the sampling counter)
@@ -240,9 +250,12 @@ static size_t layout(dvi_ctx *x, const dvi_config &c, void *base) {
         x->h = h; x->ss = ss; x->hg = hg; x->q = q; x->attn_o = attn_o; x->act = act; x->sinv_rows = sinv_rows;
         x->hk = hk; x->hk_ss = hk_ss; x->hk_hg = hk_hg; x->hk_hat = hk_hat;
         x->dfm = dfm; x->pfm = pfm; x->ufm = ufm;
-        x->vlogits = vlogits; x->dlogits = dlogits; x->part_val = part_val; x->part_idx = part_idx;
+        x->vlogits = vlogits; x->dlogits = dlogits;
         x->lora_u = lora_u;
-        x->att_po = att_po; x->att_pml = att_pml; x->att_cnt = att_cnt; x->chunk_stride = (int)cs;
+        x->ws_scr.att_po = att_po; x->ws_scr.att_pml = att_pml; x->ws_scr.att_cnt = att_cnt;
+        x->ws_scr.chunk_stride = (int)cs; x->ws_scr.part_val = part_val; x->ws_scr.part_idx = part_idx;
+        x->scr = x->ws_scr;
+        x->chunk_stride = (int)cs;
         x->lens = lens; x->pending = pending; x->drafts = drafts; x->targets = targets; x->forced = forced;
         x->max_new = max_new; x->ids = ids; x->copy_list = copy_list; x->ring_state = ring_state; x->rng_step = rng_step; x->io = io;
         x->steps_io = steps_io;
@@ -405,7 +418,7 @@ extern "C" dvi_status dvi_create(const dvi_config *cfg, const dvi_weights *w, vo
             {x->lens, (size_t)c.max_batch * 4}, {x->pending, (size_t)c.max_batch * 4}, {x->drafts, Bk * 4},
             {x->targets, Bk * 4}, {x->io, (Bk + 2 * (size_t)c.max_batch + 4) * 4}, {x->ring_state, 16}, {x->rng_step, 16},
             {x->ring_fresh, R}, {x->ring_r, R}, {x->mA, (size_t)V * r * 4}, {x->vA, (size_t)V * r * 4},
-            {x->mB, r * d * 4}, {x->vB, r * d * 4}, {x->att_cnt, (size_t)c.max_batch * c.n_kv_heads * 4}};
+            {x->mB, r * d * 4}, {x->vB, r * d * 4}, {x->ws_scr.att_cnt, (size_t)c.max_batch * c.n_kv_heads * 4}};
         for (const Z &z : zs)
             if (hipMemset(z.p, 0, z.n) != hipSuccess) {
                 *out = x;
@@ -555,10 +568,10 @@ static dvi_status run_layers(dvi_ctx *x, int l0, int l1, int B, int c, int pos_o
         at.s_max = x->s_cap;
         at.scale = 1.0f / sqrtf((float)hd);
         at.n_chunks = n_chunks;
-        at.chunk_stride = x->chunk_stride;
-        at.part_o = x->att_po;
-        at.part_ml = x->att_pml;
-        at.counters = x->att_cnt;
+        at.chunk_stride = x->scr.chunk_stride;
+        at.part_o = x->scr.att_po;
+        at.part_ml = x->scr.att_pml;
+        at.counters = x->scr.att_cnt;
         at.O = x->attn_o;
         const LaunchEvents ev = probe_begin(x, DVI_PROBE_ATTENTION);
         launch_attention(x->dt, at, x->stream, ev);
@@ -623,8 +636,8 @@ static void head(dvi_ctx *x, const void *X, const float *ss_in, int ld_ss, int M
     a.ld_ss_in = ld_ss;
     a.eps = cf.rms_eps;
     a.Z = Z;
-    a.part_val = x->part_val;
-    a.part_idx = x->part_idx;
+    a.part_val = x->scr.part_val;
+    a.part_idx = x->scr.part_idx;
     if (lora) {
         a.lora_A = x->lora_A;
         a.lora_u = x->lora_u;
@@ -632,7 +645,7 @@ static void head(dvi_ctx *x, const void *X, const float *ss_in, int ld_ss, int M
         a.gamma = cf.lora_gamma;
     }
     gemm(x, EPI_LOGITS, DVI_PROBE_HEAD, x->head, X, M, cf.vocab, cf.d_model, a);
-    launch_argmax(x->part_val, x->part_idx, M, cf.vocab / 16, out, out_stride, forced, flags_ptr(x), x->stream);
+    launch_argmax(x->scr.part_val, x->scr.part_idx, M, cf.vocab / 16, out, out_stride, forced, flags_ptr(x), x->stream);
 }
 
 static void ev_begin(dvi_ctx *x, int phase) {
@@ -704,14 +717,20 @@ extern "C" dvi_status dvi_prefill(dvi_ctx *x, int32_t batch, const int32_t *ids,
     if (!ids || !lens || !first_tok) return fail(x, DVI_ERR_ARG, "null argument");
     if (batch < 1) return fail(x, DVI_ERR_ARG, "batch < 1");
     if (batch > cf.max_batch) return fail(x, DVI_ERR_CAPACITY, "batch %d > max_batch %d", batch, cf.max_batch);
-    const int P = lens[0];
+    // Prompts may differ in length: every sequence runs over P = the longest prompt, the shorter
+    // ones padded with token 0 at the end.  A row attends only to positions at or before its own,
+    // so padding changes no real row; its keys and values lie past the sequence's length, where
+    // decoding overwrites them before any row can read them.
+    int P = 0;
+    for (int b = 0; b < batch; ++b) {
+        if (lens[b] < 1 || lens[b] > stride) return fail(x, DVI_ERR_ARG, "prompt length %d of sequence %d outside [1, stride]", lens[b], b);
+        if (lens[b] + 1 > cf.max_seq)
+            return fail(x, DVI_ERR_CAPACITY, "prompt length %d leaves no room in max_seq %d", lens[b], cf.max_seq);
+        P = lens[b] > P ? lens[b] : P;
+    }
+    std::vector<int32_t> packed((size_t)batch * P, 0);
     for (int b = 0; b < batch; ++b)
-        if (lens[b] != P) return fail(x, DVI_ERR_ARG, "prompt lengths must be equal");
-    if (P < 1 || P > stride) return fail(x, DVI_ERR_ARG, "prompt length must be in [1, stride]");
-    if (P + 1 > cf.max_seq) return fail(x, DVI_ERR_CAPACITY, "prompt length %d leaves no room in max_seq %d", P, cf.max_seq);
-    std::vector<int32_t> packed((size_t)batch * P);
-    for (int b = 0; b < batch; ++b)
-        for (int i = 0; i < P; ++i) {
+        for (int i = 0; i < lens[b]; ++i) {
             const int32_t t = ids[(size_t)b * stride + i];
             if (t < 0 || t >= cf.vocab) return fail(x, DVI_ERR_ARG, "token id %d out of range", t);
             packed[(size_t)b * P + i] = t;
@@ -733,20 +752,27 @@ extern "C" dvi_status dvi_prefill(dvi_ctx *x, int32_t batch, const int32_t *ids,
             run_layers(x, 0, cf.n_layers, batch, cc, s0, attn_chunks(x, s0 + cc - 1), x->h, x->ss, x->hg, 1, x->hg, 1, 0,
                        true);
         if (st != DVI_OK) return st;
-        if (s0 + cc == P) {  // last prompt token of every sequence -> first generated token
-            launch_gather_fm(x->dt, x->hg, true, cc, cc - 1, batch, d, x->pfm, x->stream);
-            head(x, x->pfm, x->ss + (size_t)(cc - 1) * nps, cc * nps, batch, x->vlogits, false, x->pending, 1, nullptr);
+        // each sequence's last prompt token -> its first generated token: collect the head's
+        // input rows (pfm, with their sums of squares in hk_ss) from the block that holds them
+        LastRows lr;
+        bool any = false;
+        for (int b = 0; b < kMaxBatch; ++b) {
+            const int i = b < batch ? lens[b] - 1 - s0 : -1;
+            lr.src[b] = (i >= 0 && i < cc) ? i : -1;
+            any = any || lr.src[b] >= 0;
         }
+        if (any) launch_gather_last(x->dt, x->hg, x->ss, cc, d, nps, batch, lr, x->pfm, x->hk_ss, x->stream);
     }
+    head(x, x->pfm, x->hk_ss, nps, batch, x->vlogits, false, x->pending, 1, nullptr);
     std::vector<int32_t> lh(cf.max_batch, 0);
-    for (int b = 0; b < batch; ++b) lh[b] = P;
+    for (int b = 0; b < batch; ++b) lh[b] = lens[b];
     HIPCHK(x, hipMemcpyAsync(x->lens, lh.data(), cf.max_batch * 4, hipMemcpyHostToDevice, x->stream));
     int32_t fl[4];
     HIPCHK(x, hipMemcpyAsync(first_tok, x->pending, batch * 4, hipMemcpyDeviceToHost, x->stream));
     HIPCHK(x, hipMemcpyAsync(fl, flags_ptr(x), 16, hipMemcpyDeviceToHost, x->stream));
     HIPCHK(x, hipStreamSynchronize(x->stream));
     LAUNCHCHK(x);
-    for (int b = 0; b < batch; ++b) x->lens_h[b] = P;
+    for (int b = 0; b < batch; ++b) x->lens_h[b] = lens[b];
     x->k_spec = 1;  // dvi_read_logits now returns the prefill's head logits, one row per sequence
     x->state = S_READY;
     if (fl[0]) return fail(x, DVI_ERR_NUMERIC, "non-finite logits in prefill");
@@ -792,14 +818,15 @@ static dvi_status draft_pass(dvi_ctx *x, int k_spec, bool forced, int nck) {
 static dvi_status verify_pass(dvi_ctx *x, int nck) {
     const dvi_config &cf = x->cfg;
     const int B = x->B, k = x->k_spec, M = B * k, d = cf.d_model;
-    const dvi_status st = run_pass(x, {1, B, k, 0, nck}, [&]() -> dvi_status {
+    auto body = [&]() -> dvi_status {
         dvi_status sl =
             run_layers(x, cf.split_k, cf.n_layers, B, k, 0, nck, x->hk, x->hk_ss, x->hk_hg, 1, x->hk_hg, 1, 0);
         if (sl != DVI_OK) return sl;
         head(x, x->hk_hg, x->hk_ss, d / 16, M, x->vlogits, false, x->targets, 1, nullptr);
         LAUNCHCHK(x);
         return DVI_OK;
-    });
+    };
+    const dvi_status st = run_pass(x, {1, B, k, 0, nck}, body);
     if (st != DVI_OK) return st;
     LAUNCHCHK(x);
     return DVI_OK;
@@ -1056,8 +1083,8 @@ extern "C" dvi_status dvi_update_drafter(dvi_ctx *x, const dvi_update_args *ua, 
     u.Bm = x->lora_B;
     u.u = x->upd_u;
     u.Z = x->upd_Z;
-    u.part_val = x->part_val;
-    u.part_idx = x->part_idx;
+    u.part_val = x->ws_scr.part_val;
+    u.part_idx = x->ws_scr.part_idx;
     u.row_stats = x->upd_stats;
     u.dA = x->upd_dA;
     u.du = x->upd_du;

@@ -131,6 +131,17 @@ void launch_gather_fm(DType t, const void *src, bool src_fm, int rs, int off, in
 
 constexpr int kMaxBatch = 64;
 
+// Rows of one prefill block that hold a sequence's last prompt token: src[b] = the row within
+// the block of sequence b's last token (row b * block_len + src[b]), or -1 when that token lies in
+// another block.
+struct LastRows {
+    int32_t src[kMaxBatch];
+};
+// For every sequence b with src[b] >= 0: FM row b of dst <- FM row (b * block_len + src[b]) of
+// hg (K = d columns), and row b of ss_dst <- that row of ss (nps partial sums each).
+void launch_gather_last(DType t, const void *hg, const float *ss, int block_len, int d, int nps, int B,
+                        const LastRows &lr, void *dst, float *ss_dst, hipStream_t s);
+
 struct AttnArgs {
     const float *Q;      // [M][n_heads*hd]
     const void *Kc;      // [max_batch][n_kv][s_max / 64][block], blocks as kv_key_offset

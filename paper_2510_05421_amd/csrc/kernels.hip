@@ -498,6 +498,29 @@ void launch_gather_fm(DType t, const void *src, bool src_fm, int rs, int off, in
         gather_fm_kernel<DType::F32><<<rows, 256, 0, s>>>(src, src_fm ? 1 : 0, rs, off, K, dst);
 }
 
+// The prefill's head input when prompts differ in length: each sequence's last prompt row of a
+// block (its folded-norm input dtype(h * g_final) and the row's partial sums of squares) goes to
+// row b of compact buffers.  Workgroup b.
+template <DType T>
+__global__ void __launch_bounds__(256) gather_last_kernel(const void *hg, const float *ss, int block_len, int d,
+                                                          int nps, LastRows lr, void *dst, float *ss_dst) {
+    const int b = blockIdx.x;
+    const int i = lr.src[b];
+    if (i < 0) return;  // uniform across the workgroup
+    const int r = b * block_len + i;
+    for (int k = threadIdx.x; k < d; k += 256) St<T>::store(dst, fm_index<T>(b, k, d), St<T>::load(hg, fm_index<T>(r, k, d)));
+    for (int k = threadIdx.x; k < nps; k += 256) ss_dst[(size_t)b * nps + k] = ss[(size_t)r * nps + k];
+}
+
+void launch_gather_last(DType t, const void *hg, const float *ss, int block_len, int d, int nps, int B,
+                        const LastRows &lr, void *dst, float *ss_dst, hipStream_t s) {
+    if (B <= 0) return;
+    if (t == DType::BF16)
+        gather_last_kernel<DType::BF16><<<B, 256, 0, s>>>(hg, ss, block_len, d, nps, lr, dst, ss_dst);
+    else
+        gather_last_kernel<DType::F32><<<B, 256, 0, s>>>(hg, ss, block_len, d, nps, lr, dst, ss_dst);
+}
+
 // u[m][c] = sum_i B_s[c][i] x[m][i] for already-normalised rows x.  Workgroup (c, m).
 template <DType T>
 __global__ void __launch_bounds__(256) lora_u_kernel(const void *x, const float *Bm, int d, int r, float *u) {

@@ -167,12 +167,14 @@ class Engine:
         return getattr(self.lib, fn)(self.ctx, *args)
 
     # ------------------------------------------------------------------ decode step
-    def prefill(self, ids) -> np.ndarray:
+    def prefill(self, ids, lens=None) -> np.ndarray:
+        """ids [B, P]; lens [B] (default: P for every sequence) -- sequence b's prompt is
+        ids[b, :lens[b]]."""
         ids = _i32(ids)
         if ids.ndim == 1:
             ids = ids[None]
         B, P = ids.shape
-        lens = np.full(B, P, np.int32)
+        lens = np.full(B, P, np.int32) if lens is None else _i32(lens).reshape(B)
         first = np.empty(B, np.int32)
         st = self.lib.dvi_prefill(self.ctx, B, ids.ctypes.data, lens.ctypes.data, P, first.ctypes.data)
         if st in (_abi.OK, _abi.ERR_NUMERIC):  # the prefill ran (a non-finite head logit is reported after it)
@@ -304,13 +306,13 @@ class Engine:
 
     # ------------------------------------------------------------------ driver
     def generate(self, prompts, n_new: int, k_spec: int, update_every: int = 0,
-                 schedule: Optional[KLRLSchedule] = None, lr: float = 1e-3, on_step=None):
+                 schedule: Optional[KLRLSchedule] = None, lr: float = 1e-3, on_step=None, lens=None):
         """Prefill then decode until every sequence has n_new tokens (the first from the prefill).
 
         Returns (tokens [B, n_new], info) with per-step accept lengths m and commit counts n.
         update_every > 0 runs a drafter update after every update_every decode steps, with
-        coefficients from the KL->RL schedule."""
-        first = self.prefill(prompts)
+        coefficients from the KL->RL schedule.  lens: per-sequence prompt lengths (see prefill)."""
+        first = self.prefill(prompts, lens)
         B = self.batch
         out: List[List[int]] = [[int(t)] for t in first]
         remaining = np.full(B, n_new - 1, np.int32)
