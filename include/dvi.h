@@ -166,6 +166,22 @@ dvi_status dvi_draft(dvi_ctx *ctx, int32_t k_spec, const int32_t *forced, int32_
 dvi_status dvi_verify(dvi_ctx *ctx, int32_t *targets_out, int32_t *accept_out);
 
 /*
+ * dvi_verify for callers that cannot allocate device memory: code under HIP graph capture, tight
+ * serving loops, harnesses that forbid allocation.  Same semantics, arguments and results as
+ * dvi_verify (bit for bit), but its device scratch (attention partials and merge counters, the
+ * head's argmax partials) lives in a static array of the library, one 16 MiB copy per device that
+ * the library holds until the process ends, instead of in the workspace; its kernels are launched
+ * directly (no graph instantiation), and it calls no hipMalloc/hipFree.  Every context on a device
+ * shares that device's array and the array keeps the last call's contents (the counters are
+ * cleared by a kernel at the start of each call): calls that overlap on one device race.
+ * DVI_ERR_CAPACITY, before anything is launched, when the step needs more scratch than the array
+ * holds (batch*k_spec * n_heads * 64-key chunks of the longest sequence * (head_dim + 2) * 4 bytes
+ * of attention partials, plus batch*k_spec * vocab/2 bytes); DVI_ERR_DEVICE if the array's address
+ * could not be resolved on this device.  DRAFTED -> VERIFIED
+ */
+dvi_status dvi_verify_static(dvi_ctx *ctx, int32_t *targets_out, int32_t *accept_out);
+
+/*
  * Commit (Section 3.3): per sequence m = longest agreeing prefix,
  * n = min(m+1, k_spec, max_new[b]) tokens y*_{t+1..t+n} are committed, the
  * cache length advances by n (keys/values beyond it are stale and are

@@ -51,6 +51,7 @@ SIGNATURES = {
     "dvi_prefill": (c_i32, [c_vp, c_i32, c_vp, c_vp, c_i32, c_vp]),
     "dvi_draft": (c_i32, [c_vp, c_i32, c_vp, c_vp]),
     "dvi_verify": (c_i32, [c_vp, c_vp, c_vp]),
+    "dvi_verify_static": (c_i32, [c_vp, c_vp, c_vp]),
     "dvi_commit": (c_i32, [c_vp, c_vp, c_vp, c_vp, c_vp, c_vp]),
     "dvi_decode_steps": (c_i32, [c_vp, c_i32, c_i32, c_vp, c_vp, c_vp, c_vp]),
     "dvi_abort_step": (c_i32, [c_vp]),

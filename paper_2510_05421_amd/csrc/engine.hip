@@ -12,6 +12,7 @@
 #include <algorithm>
 #include <array>
 #include <map>
+#include <mutex>
 #include <vector>
 
 #include "../../include/dvi.h"
@@ -77,8 +78,11 @@ struct dvi_ctx {
     float *sinv_rows;  // 1/rms per token for prefill-block GEMMs
     int chunk_stride = 0;  // 64-key chunks of the longest sequence (max_seq), the attention grid's cap
     void *hg, *attn_o, *act, *hk_hg, *hk_hat, *dfm, *pfm, *ufm;
-    // scratch in the workspace (ws_scr), and the scratch the launches use (scr)
+    // scratch in the workspace (ws_scr), and the scratch the launches use (scr): ws_scr, except
+    // inside dvi_verify_static, which points it at the library's static device array
     Scratch ws_scr, scr;
+    int dev = 0;            // device current at dvi_create
+    void *static_scratch = nullptr;  // that device's copy of the static array (nullptr: unresolved)
     // small device state; io block is one contiguous region copied back at commit
     int32_t *lens, *pending, *drafts, *targets, *forced, *max_new, *ids, *copy_list, *ring_state;
     int32_t *rng_step;  // [0]: decode steps committed since the prefill (the sampling counter)
@@ -143,6 +147,39 @@ static dvi_status fail(dvi_ctx *c, dvi_status s, const char *fmt, ...) {
     } while (0)
 
 static size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// ------------------------------------------------------------------------------------------
+// Static scratch of dvi_verify_static.  The array lives in the library's device code object, so
+// each GPU that loads the library holds its own copy until the process ends; host code reaches a
+// device's copy only through the address hipGetSymbolAddress returns for it (the array's name is a
+// host-side stand-in, not a device address).  Every context on a device shares that device's
+// copy: calls that overlap on one device race on it.
+// ------------------------------------------------------------------------------------------
+constexpr size_t kStaticScratchBytes = (size_t)16 << 20;
+static __device__ __align__(256) uint8_t scratch[kStaticScratchBytes];
+constexpr int kMaxDevices = 64;
+static std::mutex g_scratch_mu;
+static void *g_scratch_addr[kMaxDevices];  // per device: the address of its copy (nullptr: not resolved)
+
+// Resolve (once per device, with that device current) the address of the device's copy.
+static hipError_t resolve_static_scratch(int dev, void **out) {
+    *out = nullptr;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_addr[dev]) {
+        void *p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        g_scratch_addr[dev] = p;
+    }
+    *out = g_scratch_addr[dev];
+    return hipSuccess;
+}
+
+__global__ void fill_i32_kernel(int32_t *p, int n, int32_t v) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = v;
+}
 
 static int qkv_rows(const dvi_config &c) { return (c.n_heads + 2 * c.n_kv_heads) * c.head_dim; }
 static int cache_cap(const dvi_config &c) { return (c.max_seq + 63) / 64 * 64; }
@@ -341,6 +378,10 @@ extern "C" dvi_status dvi_create(const dvi_config *cfg, const dvi_weights *w, vo
     x->stream = (hipStream_t)stream;
     x->graphs = stream != nullptr;
     layout(x, *cfg, ws);
+    // the static scratch of dvi_verify_static on this device (a failure only disables that call)
+    if (hipGetDevice(&x->dev) == hipSuccess && resolve_static_scratch(x->dev, &x->static_scratch) != hipSuccess)
+        x->static_scratch = nullptr;
+    (void)hipGetLastError();
     x->lora_A = w->lora_A;
     x->lora_B = w->lora_B;
     const dvi_config &c = *cfg;
@@ -815,7 +856,7 @@ static dvi_status draft_pass(dvi_ctx *x, int k_spec, bool forced, int nck) {
 }
 
 // One verify pass (Section 3.3): layers k+1..L over the B * k_spec kept rows, then the head.
-static dvi_status verify_pass(dvi_ctx *x, int nck) {
+static dvi_status verify_pass(dvi_ctx *x, int nck, bool direct = false) {
     const dvi_config &cf = x->cfg;
     const int B = x->B, k = x->k_spec, M = B * k, d = cf.d_model;
     auto body = [&]() -> dvi_status {
@@ -826,7 +867,7 @@ static dvi_status verify_pass(dvi_ctx *x, int nck) {
         LAUNCHCHK(x);
         return DVI_OK;
     };
-    const dvi_status st = run_pass(x, {1, B, k, 0, nck}, body);
+    const dvi_status st = direct ? body() : run_pass(x, {1, B, k, 0, nck}, body);
     if (st != DVI_OK) return st;
     LAUNCHCHK(x);
     return DVI_OK;
@@ -922,6 +963,63 @@ extern "C" dvi_status dvi_verify(dvi_ctx *x, int32_t *targets_out, int32_t *acce
                 int m = 0;
                 if (!x->ar_mode)
                     while (m < k && dr[(size_t)b * k + m] == tg[(size_t)b * k + m]) ++m;
+                accept_out[b] = m;
+            }
+    }
+    x->state = S_VERIFIED;
+    return DVI_OK;
+}
+
+// Bytes of static scratch one verify of M rows over nck attention chunks takes (each piece
+// 256-byte aligned), and its layout when base is given.
+static size_t static_scratch_layout(const dvi_ctx *x, int M, int nck, void *base, Scratch *out) {
+    const dvi_config &c = x->cfg;
+    Bump b(base);
+    Scratch s;
+    s.chunk_stride = nck;
+    s.att_po = b.take<float>((size_t)M * c.n_heads * nck * c.head_dim * 4);
+    s.att_pml = b.take<float>((size_t)M * c.n_heads * nck * 2 * 4);
+    s.att_cnt = b.take<int32_t>((size_t)c.max_batch * c.n_kv_heads * 4);
+    s.part_val = b.take<float>((size_t)M * (c.vocab / 16) * 4);
+    s.part_idx = b.take<int32_t>((size_t)M * (c.vocab / 16) * 4);
+    if (out) *out = s;
+    return align_up(b.off);
+}
+
+extern "C" dvi_status dvi_verify_static(dvi_ctx *x, int32_t *targets_out, int32_t *accept_out) {
+    if (!x) return DVI_ERR_ARG;
+    if (x->device_error) return fail(x, DVI_ERR_DEVICE, "context has a sticky device error");
+    if (x->state != S_DRAFTED) return fail(x, DVI_ERR_STATE, "verify needs state DRAFTED");
+    if (!x->static_scratch) return fail(x, DVI_ERR_DEVICE, "the static scratch of device %d is not available", x->dev);
+    const int B = x->B, k = x->k_spec, M = B * k;
+    const int nck = attn_chunks(x, max_len(x) + k - 1);
+    const size_t need = static_scratch_layout(x, M, nck, nullptr, nullptr);
+    if (need > kStaticScratchBytes)
+        return fail(x, DVI_ERR_CAPACITY, "verify of %d rows over %d key chunks needs %zu bytes of static scratch; the maximum is %zu",
+                    M, nck, need, kStaticScratchBytes);
+    Scratch st_scr;
+    static_scratch_layout(x, M, nck, x->static_scratch, &st_scr);
+    // the merge counters start at zero (a kernel, not a memset, so a caller may capture this call)
+    const int ncnt = x->cfg.max_batch * x->cfg.n_kv_heads;
+    fill_i32_kernel<<<(ncnt + 255) / 256, 256, 0, x->stream>>>(st_scr.att_cnt, ncnt, 0);
+    LAUNCHCHK(x);
+    ev_begin(x, 1);
+    x->scr = st_scr;
+    const dvi_status st = verify_pass(x, nck, true);
+    x->scr = x->ws_scr;
+    if (st != DVI_OK) return st;
+    ev_end(x, 1);
+    if (targets_out || accept_out) {
+        int32_t tg[kMaxRows], dr[kMaxRows];  // M <= kMaxRows (max_batch * max_k_spec is checked at create)
+        HIPCHK(x, hipMemcpyAsync(tg, x->targets, (size_t)M * 4, hipMemcpyDeviceToHost, x->stream));
+        HIPCHK(x, hipMemcpyAsync(dr, x->drafts, (size_t)(x->ar_mode ? B : M) * 4, hipMemcpyDeviceToHost, x->stream));
+        HIPCHK(x, hipStreamSynchronize(x->stream));
+        if (targets_out) memcpy(targets_out, tg, (size_t)M * 4);
+        if (accept_out)
+            for (int b = 0; b < B; ++b) {
+                int m = 0;
+                if (!x->ar_mode)
+                    while (m < k && dr[b * k + m] == tg[b * k + m]) ++m;
                 accept_out[b] = m;
             }
     }
