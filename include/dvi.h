@@ -325,6 +325,17 @@ dvi_status dvi_set_sampling(dvi_ctx *ctx, float tau, uint64_t seed);
  */
 dvi_status dvi_set_graphs(dvi_ctx *ctx, int32_t enable);
 
+/*
+ * Streaming-read reference (measurement only): reads the caller's DEVICE buffer buf[0, bytes)
+ * reps times with the same non-temporal 16-byte loads the decode GEMMs stream their weights
+ * with, each pass timed by HIP events stamped at the kernel's own start and end, and returns the
+ * fastest pass's rate in *gb_s (1e9 bytes per second): the practical HBM read ceiling the step's
+ * kernels are compared against, beside the nominal peak.  bytes: at least 1 MiB, a multiple of
+ * 16; the buffer must exceed the last-level cache for an HBM figure.  Runs on the context's
+ * stream and synchronises it.  DVI_ERR_ARG on bad arguments.
+ */
+dvi_status dvi_measure_read_rate(dvi_ctx *ctx, const void *buf, size_t bytes, int32_t reps, double *gb_s);
+
 /* Per-phase device time of the last call of each kind (ms, hipEvent based). */
 dvi_status dvi_get_timings(dvi_ctx *ctx, double *ms_draft, double *ms_verify, double *ms_commit, double *ms_update);
 

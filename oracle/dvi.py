@@ -124,7 +124,7 @@ def dvi_generate(model: OracleModel, prompt, n_new: int, k_spec: int, drafter: D
                  forced_drafts: Optional[Callable[[int, int, np.ndarray], Optional[np.ndarray]]] = None,
                  on_step: Optional[Callable[["DVIResult", int], None]] = None,
                  s_max: Optional[int] = None, split_k: Optional[int] = None,
-                 max_steps: Optional[int] = None) -> DVIResult:
+                 max_steps: Optional[int] = None, on_prefill: Optional[Callable[[], None]] = None) -> DVIResult:
     """Run DVI draft -> verify -> commit -> log until n_new tokens are committed.
 
     forced_drafts(step, pos, committed) may return an int array [k_spec] that
@@ -132,6 +132,7 @@ def dvi_generate(model: OracleModel, prompt, n_new: int, k_spec: int, drafter: D
     on_step(result, step) is called after each commit; it may replace
     drafter.A / drafter.B (the online update), read at the next draft.
     max_steps stops after that many decode steps (bounded runs).
+    on_prefill() is called once the prompt is processed and the first token chosen (timing).
     """
     s = model.shape
     k = s.split_k if split_k is None else split_k
@@ -142,6 +143,8 @@ def dvi_generate(model: OracleModel, prompt, n_new: int, k_spec: int, drafter: D
     h = model.layers(cache, model.embed(prompt), 0, 0, L)
     z = model.target_logits(model.final_norm(h[-1:]))
     out = [int(argmax_lowest(z)[0])]
+    if on_prefill is not None:
+        on_prefill()
     length = P                   # tokens whose keys/values are in the cache
     res = DVIResult(np.zeros(0, np.int32), [], [], cache, length)
     step = 0

@@ -69,6 +69,7 @@ SIGNATURES = {
     "dvi_set_sampling": (c_i32, [c_vp, c_f32, ctypes.c_uint64]),
     "dvi_probe_kernel": (c_i32, [c_vp, c_i32]),
     "dvi_probe_read": (c_i32, [c_vp, c_vp, c_vp, c_vp]),
+    "dvi_measure_read_rate": (c_i32, [c_vp, c_vp, ctypes.c_size_t, c_i32, c_vp]),
 }
 
 _lib = None

@@ -1389,6 +1389,37 @@ extern "C" dvi_status dvi_probe_read(dvi_ctx *x, double *total_ms, int64_t *laun
     return DVI_OK;
 }
 
+extern "C" dvi_status dvi_measure_read_rate(dvi_ctx *x, const void *buf, size_t bytes, int32_t reps, double *gb_s) {
+    if (!x) return DVI_ERR_ARG;
+    if (!buf || !gb_s || reps < 1 || bytes < ((size_t)1 << 20) || bytes % 16)
+        return fail(x, DVI_ERR_ARG, "read-rate buffer must be >= 1 MiB and a multiple of 16 bytes, reps >= 1");
+    if (x->device_error) return fail(x, DVI_ERR_DEVICE, "context has a sticky device error");
+    hipEvent_t e0, e1;
+    HIPCHK(x, hipEventCreate(&e0));
+    if (hipEventCreate(&e1) != hipSuccess) {
+        (void)hipEventDestroy(e0);
+        return fail(x, DVI_ERR_DEVICE, "hipEventCreate failed");
+    }
+    double best = 0.0;
+    dvi_status st = DVI_OK;
+    for (int r = 0; r < reps && st == DVI_OK; ++r) {
+        LaunchEvents ev;
+        ev.start = e0;
+        ev.stop = e1;
+        launch_stream_read(buf, bytes, (uint32_t *)(x->rng_step + 2), x->stream, ev);
+        float ms = 0.f;
+        if (hipGetLastError() != hipSuccess || hipEventSynchronize(e1) != hipSuccess ||
+            hipEventElapsedTime(&ms, e0, e1) != hipSuccess)
+            st = fail(x, DVI_ERR_DEVICE, "read-rate pass failed");
+        else if (ms > 0.f)
+            best = std::max(best, (double)bytes / (ms * 1e-3) / 1e9);
+    }
+    (void)hipEventDestroy(e0);
+    (void)hipEventDestroy(e1);
+    if (st == DVI_OK) *gb_s = best;
+    return st;
+}
+
 extern "C" dvi_status dvi_get_timings(dvi_ctx *x, double *md, double *mv, double *mc, double *mu) {
     if (!x) return DVI_ERR_ARG;
     double *outs[4] = {md, mv, mc, mu};

@@ -222,4 +222,9 @@ void launch_update_backward(DType t, const UpdateArgs &u, hipStream_t s);
 void launch_adam(float *p, const float *g, float *m, float *v, int n, float lr, float b1, float b2,
                  float eps, int step, hipStream_t s);
 
+// Streaming-read reference: every 16-byte word of buf[0, bytes) read once with the decode GEMM's
+// non-temporal loads (bytes a multiple of 16); the XOR of everything read goes to sink[0] only
+// when it equals a value no buffer of this library holds, so nothing is stored in practice.
+void launch_stream_read(const void *buf, size_t bytes, uint32_t *sink, hipStream_t s, const LaunchEvents &ev = {});
+
 }  // namespace dvi

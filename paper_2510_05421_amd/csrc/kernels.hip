@@ -882,16 +882,23 @@ __global__ void __launch_bounds__(64 * WPB, (ONE && T == DType::BF16) ? 3 : 1) a
 
     // Without MERGE, attn_merge_kernel merges in a launch of its own and this workgroup is done.
     if (!MERGE) return;
-    // The workgroup that finishes last for (b, kv head) merges every row's chunks.
-    __builtin_amdgcn_s_waitcnt(0);  // this workgroup's partial stores have completed
+    // The workgroup that finishes last for (b, kv head) merges every row's chunks.  Ordering:
+    // every wave's partial stores complete, then the workgroup barrier, then thread 0's counter
+    // update, an agent-scope release read-modify-write that publishes the workgroup's partials
+    // (ordered before it by the barrier).  Only the workgroup that reads the final count follows
+    // it with an agent-scope acquire fence, synchronising with every earlier release of the
+    // counter; the barrier below orders that before all of its threads' merge loads.
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (threadIdx.x == 0) {
         const int nwg = (nch + WPB - 1) / WPB;
-        const int old = __hip_atomic_fetch_add(a.counters + b * a.n_kv + kvh, 1, __ATOMIC_RELAXED,
+        const int old = __hip_atomic_fetch_add(a.counters + b * a.n_kv + kvh, 1, __ATOMIC_RELEASE,
                                                __HIP_MEMORY_SCOPE_AGENT);
         is_last = (old == nwg - 1);
-        if (is_last)
+        if (is_last) {
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
             __hip_atomic_store(a.counters + b * a.n_kv + kvh, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
     }
     __syncthreads();
     if (!is_last) return;
@@ -1488,6 +1495,39 @@ void launch_adam(float *p, const float *g, float *m, float *v, int n, float lr, 
                  hipStream_t s) {
     const float c1 = 1.f - powf(b1, (float)step), c2 = 1.f - powf(b2, (float)step);
     adam_kernel<<<(n + 255) / 256, 256, 0, s>>>(p, g, m, v, n, lr, b1, b2, eps, c1, c2);
+}
+
+// ------------------------------------------------------------------------------------------
+// Streaming-read reference (measurement): the HBM read rate the decode GEMMs' load pattern can
+// reach.  Each lane streams 16-byte non-temporal loads, eight in flight, over a grid-stride range.
+// ------------------------------------------------------------------------------------------
+__global__ void __launch_bounds__(256) stream_read_kernel(const uint4 *buf, size_t n16, uint32_t *sink) {
+    constexpr int U = 8;
+    const size_t stride = (size_t)gridDim.x * blockDim.x;
+    uint32_t acc = 0;
+    size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    for (; i + (U - 1) * stride < n16; i += U * stride) {
+        uint4 v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) v[u] = ld_stream(buf + i + u * stride);
+#pragma unroll
+        for (int u = 0; u < U; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
+    }
+    for (; i < n16; i += stride) {
+        const uint4 v = ld_stream(buf + i);
+        acc ^= v.x ^ v.y ^ v.z ^ v.w;
+    }
+    if (acc == 0x9e3779b9u) sink[0] = acc;
+}
+
+void launch_stream_read(const void *buf, size_t bytes, uint32_t *sink, hipStream_t s, const LaunchEvents &ev) {
+    // eight 256-lane workgroups per compute unit
+    const int grid = compute_units() * 8;
+    if (ev.start || ev.stop)
+        hipExtLaunchKernelGGL(stream_read_kernel, dim3(grid), dim3(256), 0, s, ev.start, ev.stop, 0,
+                              (const uint4 *)buf, bytes / 16, sink);
+    else
+        stream_read_kernel<<<grid, 256, 0, s>>>((const uint4 *)buf, bytes / 16, sink);
 }
 
 }  // namespace dvi

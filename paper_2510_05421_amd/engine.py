@@ -299,6 +299,16 @@ class Engine:
         self._check(self.lib.dvi_probe_read(self.ctx, ctypes.byref(t), ctypes.byref(n), ctypes.byref(b)))
         return {"ms": t.value, "launches": n.value, "bytes": b.value}
 
+    def read_rate(self, nbytes: int, reps: int = 5) -> float:
+        """Streaming-read reference: GB/s of the fastest of reps reads of a fresh device buffer
+        (see dvi_measure_read_rate)."""
+        buf = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
+        self.stream.wait_stream(torch.cuda.current_stream(self.device))
+        v = ctypes.c_double()
+        self._check(self.lib.dvi_measure_read_rate(self.ctx, buf.data_ptr(), nbytes, reps, ctypes.byref(v)))
+        del buf
+        return v.value
+
     def timings(self) -> Dict[str, float]:
         vals = [ctypes.c_double() for _ in range(4)]
         self._check(self.lib.dvi_get_timings(self.ctx, *[ctypes.byref(v) for v in vals]))
