@@ -614,6 +614,7 @@ static dvi_status run_layers(dvi_ctx *x, int l0, int l1, int B, int c, int pos_o
         at.part_ml = x->scr.att_pml;
         at.counters = x->scr.att_cnt;
         at.O = x->attn_o;
+        at.flash = prefill ? 1 : 0;
         const LaunchEvents ev = probe_begin(x, DVI_PROBE_ATTENTION);
         launch_attention(x->dt, at, x->stream, ev);
         if (ev.start) {

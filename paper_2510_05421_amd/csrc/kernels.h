@@ -158,6 +158,9 @@ struct AttnArgs {
     float *part_ml;      // [M][n_heads][chunk_stride][2]
     int32_t *counters;   // [max_batch][n_kv]; zero between launches (the merging workgroup resets)
     void *O;             // [M][n_heads*hd] out (dtype, FM)
+    // prefill blocks: causal attention with an online softmax over each row's chunks in one kernel
+    // (no partials; part_o, part_ml, counters unused)
+    int flash;
 };
 void launch_attention(DType t, const AttnArgs &a, hipStream_t s, const LaunchEvents &ev = {});
 

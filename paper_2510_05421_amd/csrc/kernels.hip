@@ -919,6 +919,120 @@ __global__ void __launch_bounds__(256) attn_merge_kernel(AttnArgs a) {
     merge_row<T, HD>(a, m, h, (a.lens[b] + a.pos_off + i) / CK + 1, lane);
 }
 
+// Causal attention of a prefill block, flash-style: each query row's softmax runs online over its
+// 64-key chunks in increasing order, and no partials leave the workgroup.  Workgroup (tile x, kv
+// head, sequence b) of four waves; wave w owns rows r0 = 64 x + 16 w .. +15 of the R = c * G rows
+// that read this kv head (row r = i * G + gi: position len0 + i, head kvh * G + gi), as the MFMA
+// row dimension.  Per chunk: S = Q K^T, the chunk's row maxima, a rescale of the running sum and
+// output by exp(m_old - m_new), P = exp(S - m_new) through the wave's LDS tile into A-operand
+// layout, O += P V.  A row's arithmetic depends only on its position and the cache: chunks past a
+// row's position have every key masked and leave its max, sum and output exactly as they were, so
+// results do not depend on how the prompt is cut into blocks or on the rows sharing a tile.
+template <DType T, int HD>
+__global__ void __launch_bounds__(256) flash_prefill_kernel(AttnArgs a) {
+    typedef AttnTile<T, HD> A;
+    typedef typename St<T>::type E;
+    __shared__ __align__(16) E Ps[4][16][A::PST];
+    const int kvh = blockIdx.y, b = blockIdx.z;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, l16 = lane & 15, lg = lane >> 4;
+    const int G = a.n_heads / a.n_kv, R = a.c * G;
+    const int r0 = 64 * blockIdx.x + 16 * w;
+    if (r0 >= R) return;  // uniform across the wave; no workgroup barrier follows
+    const int len0 = a.lens[b] + a.pos_off;
+    const int last_ch = (len0 + min(r0 + 15, R - 1) / G) / CK;  // chunk of the tile's last position
+    const int nwritten = len0 + a.c;                             // cache positions holding keys/values
+    uint4 qf[A::DS];
+    {
+        typename A::QRaw qraw;
+        A::load_q(a, b, kvh, r0, qraw);
+        A::pack_q(qraw, r0, R, qf);
+    }
+    float m_run[4], l_run[4];
+    int rpos[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int r = r0 + 4 * lg + j;
+        m_run[j] = -INFINITY;
+        l_run[j] = 0.f;
+        rpos[j] = r < R ? len0 + r / G : -1;
+    }
+    f32x4 O[A::DT];
+#pragma unroll
+    for (int dt = 0; dt < A::DT; ++dt) O[dt] = (f32x4){0.f, 0.f, 0.f, 0.f};
+    for (int ch = 0; ch <= last_ch; ++ch) {
+        const int kbase = ch * CK;
+        f32x4 S[4];
+        {
+            typename A::KFrag kf;
+            A::load_k(a, b, kvh, ch, kf);
+            __builtin_amdgcn_sched_barrier(0);
+            A::scores(qf, kf, S);
+        }
+        typename A::VFrag vf;
+        A::load_v(a, b, kvh, ch, vf);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int nvalid = rpos[j] >= 0 ? min(CK, rpos[j] + 1 - kbase) : 0;
+            float mx = -INFINITY;
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                const float sv = (16 * t + l16 < nvalid) ? S[t][j] * a.scale : -INFINITY;
+                S[t][j] = sv;
+                mx = fmaxf(mx, sv);
+            }
+#pragma unroll
+            for (int o = 1; o < 16; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+            const float mnew = fmaxf(m_run[j], mx);
+            const float alpha = mnew == -INFINITY ? 1.f : expf(m_run[j] - mnew);
+            float ps = 0.f;
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                const float pv = mnew == -INFINITY ? 0.f : expf(S[t][j] - mnew);
+                S[t][j] = pv;
+                ps += pv;
+            }
+#pragma unroll
+            for (int o = 1; o < 16; o <<= 1) ps += __shfl_xor(ps, o);
+            l_run[j] = l_run[j] * alpha + ps;
+            m_run[j] = mnew;
+#pragma unroll
+            for (int dt = 0; dt < A::DT; ++dt) O[dt][j] *= alpha;
+        }
+        // P -> LDS (row-major, dtype), then back as A fragments
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) St<T>::store(&Ps[w][4 * lg + j][0], 16 * t + l16, S[t][j]);
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        uint4 pf[A::KS];
+#pragma unroll
+        for (int ks = 0; ks < A::KS; ++ks) pf[ks] = *(const uint4 *)&Ps[w][l16][ks * A::KC + A::EPL * lg];
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        // keys past the written positions may hold anything: their values enter as zeros
+        const int nk = min(CK, nwritten - kbase);
+#pragma unroll
+        for (int dt = 0; dt < A::DT; ++dt)
+#pragma unroll
+            for (int ks = 0; ks < A::KS; ++ks)
+                O[dt] = St<T>::mma(pf[ks], mask_keys<T>(vf[dt][ks], ks * A::KC + A::EPL * lg, nk), O[dt]);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int r = r0 + 4 * lg + j;
+        if (r >= R) continue;
+        const int i = r / G, gi = r - i * G;
+        const int m = b * a.c + i, h = kvh * G + gi;
+#pragma unroll
+        for (int dt = 0; dt < A::DT; ++dt)
+            St<T>::store(a.O, fm_index<T>(m, h * HD + 16 * dt + l16, a.n_heads * HD), O[dt][j] / l_run[j]);
+    }
+}
+
 template <DType T, int HD>
 static void launch_attention_t(const AttnArgs &a, hipStream_t s, const LaunchEvents &ev) {
     // One wave per 64-key chunk, four chunks per workgroup: the workgroup that finishes last
@@ -929,8 +1043,12 @@ static void launch_attention_t(const AttnArgs &a, hipStream_t s, const LaunchEve
     // otherwise every workgroup would wait for its partial stores before counting itself done,
     // and the last merges would run at the kernel's tail, each wave merging several rows one
     // after another (6 rows: 17.1 -> 16.0 us, 20 rows: 18.6 -> 15.7 us with the second launch).
-    const long waves = (long)a.n_chunks * a.n_kv * a.B;
     const int rows = a.c * (a.n_heads / a.n_kv);
+    if (a.flash) {
+        launch_timed(flash_prefill_kernel<T, HD>, dim3((rows + 63) / 64, a.n_kv, a.B), dim3(256), s, ev, a);
+        return;
+    }
+    const long waves = (long)a.n_chunks * a.n_kv * a.B;
     if (waves >= kAttnLargeGrid || rows > 4) {
         const int all_rows = a.B * a.c * a.n_heads;
         LaunchEvents e1 = ev, e2 = ev;  // one interval around both launches
