@@ -106,6 +106,8 @@ def main():
                     help="buffer of the streaming-read reference (the measured HBM ceiling); 0 skips it")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-ar", action="store_true")
+    ap.add_argument("--no-full-update", action="store_true",
+                    help="skip timing the drafter update over a full replay ring")
     ap.add_argument("--no-device-steps", action="store_true",
                     help="skip the leg that runs the decode loop through dvi_decode_steps")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
@@ -248,6 +250,29 @@ def main():
                "head_bytes": shape.vocab * shape.d_model * (2 if shape.bf16 else 4)}
         log("drafter update: %d updates, median %.3f ms over %d rows: %.1f GFLOP -> %.1f TFLOP/s (%.3f of %g)"
             % (len(st["update_ms"]), u_ms, rows, flops / 1e9, tfs, tfs / peak, peak))
+
+    # the drafter update over a full ring (the workload's 256-row buffer): random-weight trajectories
+    # accept too few drafts to fill it within the timed window, so its rows are synthetic here
+    upd_full = None
+    if wl.update_every and not args.no_full_update:
+        R = wl.buffer_rows
+        buf = synth.make_buffer(shape.d_model, shape.vocab, R, seed=11)
+        eng.write_buffer(buf.h, buf.a, buf.logits, buf.r, buf.fresh)
+        c = sched.coeffs(eng.updates, eng.baseline)
+        times = []
+        for _ in range(6):
+            eng.update_drafter(c["c_kl"], c["c_ce"], c["c_pg"], c["c_ent"], c["tau"], eng.baseline, lr=0.0)
+            times.append(eng.timings()["update"])
+        u_ms = float(np.median(times[1:]))
+        V, d, r = shape.vocab, shape.d_model, shape.lora_rank
+        flops = 2.0 * R * V * (d + r) + 2.0 * (V * r * R + R * V * r + r * d * R)
+        gemm_flops = 2.0 * R * V * d
+        peak = 2500.0 if shape.bf16 else 157.3
+        upd_full = {"rows": R, "ms": round(u_ms, 4), "gflop": round(flops / 1e9, 2),
+                    "tflop_s": round(flops / (u_ms * 1e-3) / 1e12, 2), "mfma_peak_tflop_s": peak,
+                    "frac": round(flops / (u_ms * 1e-3) / 1e12 / peak, 4), "forward_gemm_gflop": round(gemm_flops / 1e9, 2)}
+        log("drafter update over a full %d-row ring: %.3f ms, %.1f GFLOP -> %.1f TFLOP/s (%.3f of %g)"
+            % (R, u_ms, flops / 1e9, upd_full["tflop_s"], upd_full["frac"], peak))
 
     # dominant kernel: every launch of one kernel class timed with HIP events on the engine's stream
     # (a sequence that has all its tokens keeps computing with its commits masked, so the
@@ -422,6 +447,7 @@ def main():
         "device_steps": dev,
         "prefill": prefill,
         "drafter_update": upd,
+        "drafter_update_full_ring": upd_full,
         "paper_context": PAPER_CONTEXT,
     }
     print(json.dumps(out), flush=True)

@@ -423,7 +423,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &a, int nt, const f
                 }
                 bad |= ob;
             }
-            if (valid && G4 == 0) {
+            if (valid && G4 == 0 && a.part_val != nullptr) {  // argmax partials (heads only)
                 const int nt16 = a.N / 16;
                 a.part_val[(size_t)m * nt16 + nt] = best;
                 a.part_idx[(size_t)m * nt16 + nt] = bidx | (bad << 30);

@@ -249,15 +249,151 @@ __global__ void __launch_bounds__(256) gemm_big_kernel(GemmArgs a) {
     }
 }
 
+// ------------------------------------------------------------------------------------------
+// Large-M GEMM staged through LDS (prefill blocks, the drafter update's replay rows).  Workgroup
+// tile: 128 tokens x 256 features, four waves as 2 x 2, wave (wy, wx) owning tokens 64 wy .. +63
+// (four 16-token groups) and features 128 wx .. +127 (eight tiles): 32 MFMA tiles.  Per K chunk
+// the workgroup needs 8 activation and 16 weight fragments (1 KiB each, fragment-major in memory
+// and kept so in LDS).  They travel from memory straight into an LDS ring of NS stages with
+// direct-to-LDS loads (each wave loads 6 fragments of every stage), so NS - 1 chunks are in flight
+// while one is multiplied; each wave reads its 4 + 8 fragments of the chunk from LDS.  The waits
+// are explicit: the wave's own ring loads by count (vmcnt), then a workgroup barrier, and the LDS
+// reads are issued as instructions whose completion the wave awaits itself (the compiler would
+// otherwise wait for every ring load before any LDS read).  Every output accumulates its K chunks
+// in increasing order, one MFMA per chunk: the same chain as gemm_big_kernel, so the two give the
+// same bits.  Rows or tiles past M or N load clamped (valid) fragments whose products are never
+// stored.  Workgroups are numbered so that each XCD (workgroup id mod 8) takes a contiguous range
+// of tiles, feature block major and token tile minor: consecutive workgroups of one XCD share a
+// weight block through its L2.
+// ------------------------------------------------------------------------------------------
+constexpr int kLdsStages = 4;
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    // gfx9 s_waitcnt immediate: vmcnt in bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8 (others at max)
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xf << 8));
+}
+
+typedef __attribute__((address_space(3))) uint8_t lds_u8;
+
+// 16 bytes of LDS at byte address addr + OFF, and the wait for all of a wave's LDS reads; the
+// wait names the loaded registers so nothing that uses them can move above it.
+typedef unsigned v4u32 __attribute__((ext_vector_type(4)));
+
+template <int OFF>
+__device__ __forceinline__ v4u32 lds_read16(uint32_t addr) {
+    v4u32 v;
+    asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "i"(OFF));
+    return v;
+}
+
+__device__ __forceinline__ uint4 as_uint4(v4u32 v) { return uint4{v.x, v.y, v.z, v.w}; }
+
+template <DType T, int EPI>
+__global__ void __launch_bounds__(256) gemm_lds_kernel(GemmArgs a, int n_tok_tiles, int n_tiles_total) {
+    constexpr int NS = kLdsStages, FR = 24, PER = FR / 4;  // stages, fragments per stage, per wave
+    constexpr uint32_t kStage = FR * 1024;
+    __shared__ __align__(1024) uint4 ring[NS][FR][64];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wy = wave >> 1, wx = wave & 1;
+    const int KC = (T == DType::BF16) ? 32 : 16;
+    const int KT = a.K / KC, NT = a.N / 16, NG = (a.M + 15) / 16;
+    // workgroup -> (token tile, feature block): XCD x = id % 8 takes tiles [x * per, (x+1) * per)
+    const int per = (n_tiles_total + 7) / 8;
+    const int j = blockIdx.x >> 3;
+    const int tl = (blockIdx.x & 7) * per + j;
+    if (j >= per || tl >= n_tiles_total) return;  // uniform across the workgroup (before any barrier)
+    const int g0 = (tl % n_tok_tiles) * 8, t0 = (tl / n_tok_tiles) * 16;
+    // the fragments this wave loads into every stage: f = PER * wave + i; f < 8: activation group
+    // g0 + f, else weight tile t0 + f - 8 (clamped into range)
+    const uint4 *src[PER];
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+        const int f = PER * wave + i;
+        src[i] = (f < 8 ? (const uint4 *)a.X + (size_t)min(g0 + f, NG - 1) * KT * 64
+                        : (const uint4 *)a.W + (size_t)min(t0 + f - 8, NT - 1) * KT * 64) + lane;
+    }
+    lds_u8 *const ring0 = (lds_u8 *)&ring[0][0][0];
+    auto issue = [&](int st, int k) {
+#pragma unroll
+        for (int i = 0; i < PER; ++i)
+            __builtin_amdgcn_global_load_lds((const void *)(src[i] + (size_t)k * 64),
+                                             (__attribute__((address_space(3))) void *)(ring0 + st * kStage + (PER * wave + i) * 1024),
+                                             16, 0, 0);
+    };
+    // this lane's LDS byte address in fragment 0 of stage 0; fragment f of stage st is f KiB and
+    // st stages further
+    const uint32_t lbase = (uint32_t)(uintptr_t)ring0 + 16 * lane;
+    f32x4 acc[8][4];
+#pragma unroll
+    for (int t = 0; t < 8; ++t)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) acc[t][g] = (f32x4){0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int st = 0; st < NS - 1; ++st)
+        if (st < KT) issue(st, st);
+    for (int k = 0; k < KT; ++k) {
+        // chunk k's loads are done once at most min(NS - 2, KT - 1 - k) later stages are in flight
+        const int later = min(NS - 2, KT - 1 - k);
+        static_assert(NS - 2 <= 4, "wait cases");
+        if (later >= 4) wait_vmcnt<4 * PER>();
+        else if (later == 3) wait_vmcnt<3 * PER>();
+        else if (later == 2) wait_vmcnt<2 * PER>();
+        else if (later == 1) wait_vmcnt<PER>();
+        else wait_vmcnt<0>();
+        // every wave's fragments of chunk k are in LDS, and every wave is done with the stage the
+        // next issue overwrites (its LDS reads of chunk k - 1 completed before its MFMAs)
+        __builtin_amdgcn_s_barrier();
+        if (k + NS - 1 < KT) issue((k + NS - 1) % NS, k + NS - 1);
+        const uint32_t sb = lbase + (uint32_t)(k % NS) * kStage;
+        const uint32_t xa = sb + 4 * wy * 1024, wa = sb + (8 + 8 * wx) * 1024;
+        v4u32 x0 = lds_read16<0>(xa), x1 = lds_read16<1024>(xa), x2 = lds_read16<2048>(xa), x3 = lds_read16<3072>(xa);
+        v4u32 w0 = lds_read16<0>(wa), w1 = lds_read16<1024>(wa), w2 = lds_read16<2048>(wa), w3 = lds_read16<3072>(wa);
+        v4u32 w4 = lds_read16<4096>(wa), w5 = lds_read16<5120>(wa), w6 = lds_read16<6144>(wa), w7 = lds_read16<7168>(wa);
+        asm volatile("s_waitcnt lgkmcnt(0)"
+                     : "+v"(x0), "+v"(x1), "+v"(x2), "+v"(x3), "+v"(w0), "+v"(w1), "+v"(w2), "+v"(w3), "+v"(w4),
+                       "+v"(w5), "+v"(w6), "+v"(w7));
+        const uint4 xf[4] = {as_uint4(x0), as_uint4(x1), as_uint4(x2), as_uint4(x3)};
+        const uint4 wf[8] = {as_uint4(w0), as_uint4(w1), as_uint4(w2), as_uint4(w3),
+                             as_uint4(w4), as_uint4(w5), as_uint4(w6), as_uint4(w7)};
+#pragma unroll
+        for (int t = 0; t < 8; ++t)
+#pragma unroll
+            for (int g = 0; g < 4; ++g) acc[t][g] = St<T>::mma(wf[t], xf[g], acc[t][g]);
+    }
+    const int gw = g0 + 4 * wy;
+    if (gw >= NG) return;  // uniform across the wave
+    const int m0 = 16 * gw;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+        const int nt = t0 + 8 * wx + t;
+        if (nt >= NT) break;  // uniform
+        EpiOperands<4> pre;
+        epilogue_prefetch<4, EPI>(a, nt, pre, m0);
+        epilogue_prefetch_rope<4, EPI>(a, nt, pre);
+        gemm_epilogue<T, 4, EPI>(a, nt, acc[t], a.sinv_rows + m0, pre, m0);
+    }
+}
+
+template <DType T, int EPI>
+static void launch_gemm_lds(const GemmArgs &a, hipStream_t s, const LaunchEvents &ev) {
+    const int tok = (a.M + 127) / 128, blk = (a.N / 16 + 15) / 16, total = tok * blk;
+    const int grid = 8 * ((total + 7) / 8);
+    if (ev.start || ev.stop)
+        hipExtLaunchKernelGGL(gemm_lds_kernel<T, EPI>, dim3(grid), dim3(256), 0, s, ev.start, ev.stop, 0, a, tok, total);
+    else
+        gemm_lds_kernel<T, EPI><<<grid, 256, 0, s>>>(a, tok, total);
+}
+
 template <DType T>
 static void launch_gemm_big(Epi e, const GemmArgs &a, hipStream_t s, const LaunchEvents &ev) {
     if (a.ss_in != nullptr)
         rms_rows_kernel<<<(a.M + 3) / 4, 256, 0, s>>>(a.ss_in, a.ld_ss_in, a.K / 16, a.K, a.eps, a.M, a.sinv_rows);
-    const dim3 grid((a.M + 127) / 128, (a.N / 16 + 7) / 8);
     switch (e) {
-        case EPI_RESID: launch_timed(gemm_big_kernel<T, EPI_RESID>, grid, dim3(256), s, ev, a); break;
-        case EPI_QKV: launch_timed(gemm_big_kernel<T, EPI_QKV>, grid, dim3(256), s, ev, a); break;
-        case EPI_SWIGLU: launch_timed(gemm_big_kernel<T, EPI_SWIGLU>, grid, dim3(256), s, ev, a); break;
+        case EPI_RESID: launch_gemm_lds<T, EPI_RESID>(a, s, ev); break;
+        case EPI_QKV: launch_gemm_lds<T, EPI_QKV>(a, s, ev); break;
+        case EPI_SWIGLU: launch_gemm_lds<T, EPI_SWIGLU>(a, s, ev); break;
         default: break;  // the heads run on at most 64 rows (launch_gemm rejects more)
     }
 }
@@ -1470,85 +1606,10 @@ __global__ void __launch_bounds__(256) upd_dB_kernel(UpdateArgs u) {
     u.dB[(size_t)c * u.d + k] = acc;
 }
 
-// Drafter logits of the replay rows on MFMA: Z[m][v] = X[m] . W[v] + gamma * sum_c A[v][c] u[m][c]
-// for 65 to 256 rows m (X fragment-major, up to 16 groups of 16; up to 64 rows take the decode
-// GEMM, whose K split keeps each wave's chain of loads short).  A workgroup owns a band of 8
-// weight tiles (128 vocabulary rows); wave w takes tiles 2w and 2w+1 for every row group, so the
-// weights leave HBM once and each activation fragment, read by all four waves of the compute
-// unit, mostly hits L1.  Steps are software-pipelined two deep; fragments past the band or the
-// rows load a valid address and enter as zeros, so every MFMA runs unconditionally (MFMA does
-// not honour the EXEC mask).  kUpdG row groups per launch (8 or 16, the rows rounded up),
-// kUpdU steps in flight (deeper when the groups are fewer).
-constexpr int kUpdBand = 8, kUpdTW = 2;
-template <DType T, int kUpdG, int kUpdU>
-__global__ void __launch_bounds__(256) upd_gemm_kernel(const void *W, const void *X, int n, int V, int K,
-                                                       const float *A, const float *uu, int r, float gamma,
-                                                       float *Z) {
-    constexpr int KC = (T == DType::BF16) ? 32 : 16;
-    const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int KT = K / KC, NT = V / 16;
-    const int t0 = blockIdx.x * kUpdBand + kUpdTW * wave;
-    const int ng = (n + 15) / 16;
-    const uint4 zero = {0u, 0u, 0u, 0u};
-    const uint4 *wp = (const uint4 *)W + lane, *xp = (const uint4 *)X + lane;
-    f32x4 acc[kUpdTW][kUpdG];
-#pragma unroll
-    for (int t = 0; t < kUpdTW; ++t)
-#pragma unroll
-        for (int g = 0; g < kUpdG; ++g) acc[t][g] = (f32x4){0.f, 0.f, 0.f, 0.f};
-    uint4 wf[kUpdU][kUpdTW], xf[kUpdU][kUpdG];
-    auto fetch = [&](int slot, int k) {
-        const int kc = min(k, KT - 1);
-#pragma unroll
-        for (int t = 0; t < kUpdTW; ++t) {
-            const int tt = min(t0 + t, NT - 1);
-            const uint4 w = wp[((size_t)tt * KT + kc) * 64];
-            wf[slot][t] = (k < KT && t0 + t < NT) ? w : zero;
-        }
-#pragma unroll
-        for (int g = 0; g < kUpdG; ++g) {
-            const int gg = min(g, ng - 1);
-            const uint4 x = xp[((size_t)gg * KT + kc) * 64];
-            xf[slot][g] = (k < KT && g < ng) ? x : zero;
-        }
-    };
-#pragma unroll
-    for (int s = 0; s < kUpdU; ++s) fetch(s, s);
-    for (int k0 = 0; k0 < KT; k0 += kUpdU) {
-#pragma unroll
-        for (int s = 0; s < kUpdU; ++s) {
-#pragma unroll
-            for (int t = 0; t < kUpdTW; ++t)
-#pragma unroll
-                for (int g = 0; g < kUpdG; ++g) acc[t][g] = St<T>::mma(wf[s][t], xf[s][g], acc[t][g]);
-            fetch(s, k0 + s + kUpdU);
-        }
-    }
-    const int G4 = lane >> 4;
-#pragma unroll
-    for (int t = 0; t < kUpdTW; ++t) {
-        if (t0 + t >= NT) break;
-#pragma unroll
-        for (int g = 0; g < kUpdG; ++g) {
-            const int m = 16 * g + (lane & 15);
-            if (m >= n) continue;
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int v = (t0 + t) * 16 + 4 * G4 + j;
-                const float *Av = A + (size_t)v * r, *um = uu + (size_t)m * r;
-                float sl = 0.f;
-                for (int c = 0; c < r; ++c) sl += Av[c] * um[c];
-                Z[(size_t)m * V + v] = acc[t][g][j] + gamma * sl;
-            }
-        }
-    }
-}
-
 void launch_update_forward(DType t, const UpdateArgs &u, hipStream_t s) {
     float *counts = u.loss_out + 12;
     upd_counts_kernel<<<1, 64, 0, s>>>(u.r, u.fresh, u.n, counts);
     launch_lora_u(t, u.Hh, u.Bm, u.n, u.d, u.rank, u.u, s);
-    const int bands = (u.V / 16 + kUpdBand - 1) / kUpdBand;
     for (int r0 = 0; r0 < u.n; r0 += 256) {
         const int rows = min(256, u.n - r0);
         launch_gather_fm(t, u.Hh, false, 1, r0, rows, u.d, u.xfm, s);
@@ -1571,16 +1632,24 @@ void launch_update_forward(DType t, const UpdateArgs &u, hipStream_t s) {
             g.r = u.rank;
             g.gamma = u.gamma;
             launch_gemm(t, EPI_LOGITS, g, s);
-        } else if (t == DType::BF16) {
-            if (rows <= 128)
-                upd_gemm_kernel<DType::BF16, 8, 3><<<bands, 256, 0, s>>>(u.W, u.xfm, rows, u.V, u.d, u.A, ur, u.rank, u.gamma, Zr);
-            else
-                upd_gemm_kernel<DType::BF16, 16, 2><<<bands, 256, 0, s>>>(u.W, u.xfm, rows, u.V, u.d, u.A, ur, u.rank, u.gamma, Zr);
         } else {
-            if (rows <= 128)
-                upd_gemm_kernel<DType::F32, 8, 3><<<bands, 256, 0, s>>>(u.W, u.xfm, rows, u.V, u.d, u.A, ur, u.rank, u.gamma, Zr);
+            // 65 to 256 rows: the LDS-staged large-M GEMM (each workgroup 128 rows x 256
+            // vocabulary entries), its logits epilogue with the LoRA term and no argmax partials
+            GemmArgs g{};
+            g.W = u.W;
+            g.X = u.xfm;
+            g.M = rows;
+            g.N = u.V;
+            g.K = u.d;
+            g.Z = Zr;
+            g.lora_A = u.A;
+            g.lora_u = ur;
+            g.r = u.rank;
+            g.gamma = u.gamma;
+            if (t == DType::BF16)
+                launch_gemm_lds<DType::BF16, EPI_LOGITS>(g, s, LaunchEvents{});
             else
-                upd_gemm_kernel<DType::F32, 16, 2><<<bands, 256, 0, s>>>(u.W, u.xfm, rows, u.V, u.d, u.A, ur, u.rank, u.gamma, Zr);
+                launch_gemm_lds<DType::F32, EPI_LOGITS>(g, s, LaunchEvents{});
         }
     }
     upd_rows_kernel<<<u.n, 1024, 0, s>>>(u, counts);
