@@ -176,16 +176,9 @@ __global__ void __launch_bounds__(64 * WMAX) gemm_kernel(GemmArgs a) {
 }
 
 // ------------------------------------------------------------------------------------------
-// Large-M GEMM (the prefill: M = batch x prompt block, up to a few thousand tokens).
-//
-// A workgroup of four waves computes 128 tokens x 128 features; wave (wy, wx) owns tokens
-// 64 wy .. +63 (four 16-token groups) and features 64 wx .. +63 (four tiles).  Both operands
-// are fragment-major in memory, so each 16-byte load per lane is an MFMA operand as it stands:
-// per K step a wave loads four weight and four activation fragments and issues 16 MFMAs, two
-// steps in flight.  Workgroups that share a weight block are adjacent in the grid (tokens
-// fastest), so a block leaves HBM about once per XCD.  Fragments past M or N load a valid
-// address and enter as zeros: every MFMA runs unconditionally.  The epilogue is the decode
-// GEMM's, per tile, at the wave's token offset; 1/rms of each token comes from rms_rows_kernel.
+// Large-M GEMM (the prefill: M = batch x prompt block, up to a few thousand tokens; the drafter
+// update's replay rows).  1/rms of each token comes from rms_rows_kernel; the epilogue is the
+// decode GEMM's, per tile, at the wave's token offset.
 // ------------------------------------------------------------------------------------------
 __global__ void __launch_bounds__(256) rms_rows_kernel(const float *ss, int ld_ss, int nparts, int K, float eps,
                                                        int M, float *out) {
@@ -193,60 +186,6 @@ __global__ void __launch_bounds__(256) rms_rows_kernel(const float *ss, int ld_s
     if (m >= M) return;  // uniform across the wave
     const float v = inv_rms(ss + (size_t)m * ld_ss, nparts, K, eps);
     if ((threadIdx.x & 63) == 0) out[m] = v;
-}
-
-template <DType T, int EPI>
-__global__ void __launch_bounds__(256) gemm_big_kernel(GemmArgs a) {
-    constexpr int TG = 4, TF = 4, U = 2;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int wy = wave >> 1, wx = wave & 1;
-    const int KC = (T == DType::BF16) ? 32 : 16;
-    const int KT = a.K / KC, NT = a.N / 16, NG = (a.M + 15) / 16;
-    const int g0 = blockIdx.x * 8 + TG * wy, t0 = blockIdx.y * 8 + TF * wx;
-    const uint4 *Wp = (const uint4 *)a.W + lane, *Xp = (const uint4 *)a.X + lane;
-    const uint4 zero = {0u, 0u, 0u, 0u};
-    f32x4 acc[TF][TG];
-#pragma unroll
-    for (int t = 0; t < TF; ++t)
-#pragma unroll
-        for (int g = 0; g < TG; ++g) acc[t][g] = (f32x4){0.f, 0.f, 0.f, 0.f};
-    uint4 wf[U][TF], xf[U][TG];
-    auto fetch = [&](int sl, int k) {
-        const int kc = min(k, KT - 1);
-#pragma unroll
-        for (int t = 0; t < TF; ++t) {
-            const uint4 v = Wp[((size_t)min(t0 + t, NT - 1) * KT + kc) * 64];
-            wf[sl][t] = (k < KT && t0 + t < NT) ? v : zero;
-        }
-#pragma unroll
-        for (int g = 0; g < TG; ++g) {
-            const uint4 v = Xp[((size_t)min(g0 + g, NG - 1) * KT + kc) * 64];
-            xf[sl][g] = (k < KT && g0 + g < NG) ? v : zero;
-        }
-    };
-#pragma unroll
-    for (int sl = 0; sl < U; ++sl) fetch(sl, sl);
-    for (int k0 = 0; k0 < KT; k0 += U) {
-#pragma unroll
-        for (int sl = 0; sl < U; ++sl) {
-#pragma unroll
-            for (int t = 0; t < TF; ++t)
-#pragma unroll
-                for (int g = 0; g < TG; ++g) acc[t][g] = St<T>::mma(wf[sl][t], xf[sl][g], acc[t][g]);
-            fetch(sl, k0 + sl + U);
-        }
-    }
-    if (g0 >= NG) return;  // uniform across the wave
-    const int m0 = 16 * g0;
-#pragma unroll
-    for (int t = 0; t < TF; ++t) {
-        const int nt = t0 + t;
-        if (nt >= NT) break;  // uniform
-        EpiOperands<TG> pre;
-        epilogue_prefetch<TG, EPI>(a, nt, pre, m0);
-        epilogue_prefetch_rope<TG, EPI>(a, nt, pre);
-        gemm_epilogue<T, TG, EPI>(a, nt, acc[t], a.sinv_rows + m0, pre, m0);
-    }
 }
 
 // ------------------------------------------------------------------------------------------
@@ -260,9 +199,9 @@ __global__ void __launch_bounds__(256) gemm_big_kernel(GemmArgs a) {
 // are explicit: the wave's own ring loads by count (vmcnt), then a workgroup barrier, and the LDS
 // reads are issued as instructions whose completion the wave awaits itself (the compiler would
 // otherwise wait for every ring load before any LDS read).  Every output accumulates its K chunks
-// in increasing order, one MFMA per chunk: the same chain as gemm_big_kernel, so the two give the
-// same bits.  Rows or tiles past M or N load clamped (valid) fragments whose products are never
-// stored.  Workgroups are numbered so that each XCD (workgroup id mod 8) takes a contiguous range
+// in increasing order, one MFMA per chunk, whatever the tile it sits in, so a token's result does
+// not depend on M.  Rows or tiles past M or N load clamped (valid) fragments whose products are
+// never stored.  Workgroups are numbered so that each XCD (workgroup id mod 8) takes a contiguous range
 // of tiles, feature block major and token tile minor: consecutive workgroups of one XCD share a
 // weight block through its L2.
 // ------------------------------------------------------------------------------------------
