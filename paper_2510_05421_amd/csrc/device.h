@@ -57,15 +57,47 @@ __device__ __forceinline__ size_t fm_index(int m, int k, int K) {
     return ((size_t)((m >> 4) * (K / KC) + c) * 64 + G * 16 + (m & 15)) * EPL + e;
 }
 
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+// Lane exchanges inside each row of 16 lanes by DPP (a VALU operand modifier: no LDS round trip
+// and no wait, where a general shuffle goes through the LDS crossbar).  CTRL: 0xB1 = quad_perm
+// (1,0,3,2), lane l reads l^1; 0x4E = quad_perm (2,3,0,1), l^2; 0x141 = half-row mirror, lane l
+// reads the lane at 7 - (l%8) of its half-row; 0x140 = row mirror, 15 - (l%16) of its row.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+// Butterfly over each row of 16 lanes: pairs, then quads, then half-rows (the mirror pairs a lane
+// with one in the other quad), then the two halves.  Every lane of a row ends with the same
+// value, and it is bitwise the xor butterfly over 1, 2, 4, 8: at each level both partners hold
+// the same partial, so each lane adds the same two operands in the same order (own first).
+__device__ __forceinline__ float row16_sum(float v) {
+    v += dpp_f32<0xB1>(v);
+    v += dpp_f32<0x4E>(v);
+    v += dpp_f32<0x141>(v);
+    v += dpp_f32<0x140>(v);
     return v;
 }
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+__device__ __forceinline__ float row16_max(float v) {
+    v = fmaxf(v, dpp_f32<0xB1>(v));
+    v = fmaxf(v, dpp_f32<0x4E>(v));
+    v = fmaxf(v, dpp_f32<0x141>(v));
+    v = fmaxf(v, dpp_f32<0x140>(v));
     return v;
+}
+// e^x as 2^(x log2 e) on the hardware exp2 (within a few ulp), for softmax weights (x <= 0;
+// -inf gives 0, results below the normal range flush to 0).
+__device__ __forceinline__ float exp_fast(float x) { return __builtin_amdgcn_exp2f(x * 1.44269504088896341f); }
+__device__ __forceinline__ float lane_f32(float v, int lane) {  // lane must be wave-uniform
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
+}
+// Wave reductions: each row of 16 by DPP, then the four row results read out (readlane) and
+// combined as (r0 + r1) + (r2 + r3), the same tree for every lane and call.
+__device__ __forceinline__ float wave_sum(float v) {
+    v = row16_sum(v);
+    return (lane_f32(v, 0) + lane_f32(v, 16)) + (lane_f32(v, 32) + lane_f32(v, 48));
+}
+__device__ __forceinline__ float wave_max(float v) {
+    v = row16_max(v);
+    return fmaxf(fmaxf(lane_f32(v, 0), lane_f32(v, 16)), fmaxf(lane_f32(v, 32), lane_f32(v, 48)));
 }
 
 // Block-wide sum of 256 threads in a fixed order: butterfly inside each wave, then waves 0..3.
@@ -89,7 +121,7 @@ __device__ __forceinline__ float block_max256(float v, float *lds4) {
 constexpr int CK = 64;  // attention key chunk (absolute positions)
 
 // Inverse RMS of one row from its per-16-column partial sums of squares: lane l adds
-// partials l, l+64, ... in order, then a butterfly, so every lane (and every workgroup that
+// partials l, l+64, ... in order, then the wave sum, so every lane (and every workgroup that
 // asks) gets the same value.
 __device__ __forceinline__ float inv_rms(const float *ss, int nparts, int d, float eps) {
     const int lane = threadIdx.x & 63;

@@ -246,7 +246,7 @@ static size_t layout(dvi_ctx *x, const dvi_config &c, void *base) {
     float *lora_u = b.take<float>((M > R ? M : R) * r * 4);
     float *att_po = b.take<float>(Mp * c.n_heads * cs * c.head_dim * 4);
     float *att_pml = b.take<float>(Mp * c.n_heads * cs * 2 * 4);
-    int32_t *att_cnt = b.take<int32_t>((size_t)c.max_batch * c.n_kv_heads * 4);
+    int32_t *att_cnt = b.take<int32_t>((size_t)c.max_batch * c.n_kv_heads * kCounterStride * 4);
     int32_t *lens = b.take<int32_t>(c.max_batch * 4);
     int32_t *pending = b.take<int32_t>(c.max_batch * 4);
     int32_t *drafts = b.take<int32_t>(Bk * 4);
@@ -459,7 +459,7 @@ extern "C" dvi_status dvi_create(const dvi_config *cfg, const dvi_weights *w, vo
             {x->lens, (size_t)c.max_batch * 4}, {x->pending, (size_t)c.max_batch * 4}, {x->drafts, Bk * 4},
             {x->targets, Bk * 4}, {x->io, (Bk + 2 * (size_t)c.max_batch + 4) * 4}, {x->ring_state, 16}, {x->rng_step, 16},
             {x->ring_fresh, R}, {x->ring_r, R}, {x->mA, (size_t)V * r * 4}, {x->vA, (size_t)V * r * 4},
-            {x->mB, r * d * 4}, {x->vB, r * d * 4}, {x->ws_scr.att_cnt, (size_t)c.max_batch * c.n_kv_heads * 4}};
+            {x->mB, r * d * 4}, {x->vB, r * d * 4}, {x->ws_scr.att_cnt, (size_t)c.max_batch * c.n_kv_heads * kCounterStride * 4}};
         for (const Z &z : zs)
             if (hipMemset(z.p, 0, z.n) != hipSuccess) {
                 *out = x;
@@ -980,7 +980,7 @@ static size_t static_scratch_layout(const dvi_ctx *x, int M, int nck, void *base
     s.chunk_stride = nck;
     s.att_po = b.take<float>((size_t)M * c.n_heads * nck * c.head_dim * 4);
     s.att_pml = b.take<float>((size_t)M * c.n_heads * nck * 2 * 4);
-    s.att_cnt = b.take<int32_t>((size_t)c.max_batch * c.n_kv_heads * 4);
+    s.att_cnt = b.take<int32_t>((size_t)c.max_batch * c.n_kv_heads * kCounterStride * 4);
     s.part_val = b.take<float>((size_t)M * (c.vocab / 16) * 4);
     s.part_idx = b.take<int32_t>((size_t)M * (c.vocab / 16) * 4);
     if (out) *out = s;
@@ -1001,7 +1001,7 @@ extern "C" dvi_status dvi_verify_static(dvi_ctx *x, int32_t *targets_out, int32_
     Scratch st_scr;
     static_scratch_layout(x, M, nck, x->static_scratch, &st_scr);
     // the merge counters start at zero (a kernel, not a memset, so a caller may capture this call)
-    const int ncnt = x->cfg.max_batch * x->cfg.n_kv_heads;
+    const int ncnt = x->cfg.max_batch * x->cfg.n_kv_heads * kCounterStride;
     fill_i32_kernel<<<(ncnt + 255) / 256, 256, 0, x->stream>>>(st_scr.att_cnt, ncnt, 0);
     LAUNCHCHK(x);
     ev_begin(x, 1);

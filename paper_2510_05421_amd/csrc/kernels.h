@@ -156,12 +156,16 @@ struct AttnArgs {
     float scale;
     float *part_o;       // [M][n_heads][chunk_stride][hd]
     float *part_ml;      // [M][n_heads][chunk_stride][2]
-    int32_t *counters;   // [max_batch][n_kv]; zero between launches (the merging workgroup resets)
+    int32_t *counters;   // [max_batch][n_kv][kCounterStride], element 0 of each used; zero between
+                         // launches (the merging workgroup resets)
     void *O;             // [M][n_heads*hd] out (dtype, FM)
     // prefill blocks: causal attention with an online softmax over each row's chunks in one kernel
     // (no partials; part_o, part_ml, counters unused)
     int flash;
 };
+// Merge counters sit 256 bytes apart: every chunk workgroup of a (sequence, kv head) takes its
+// counter once, and counters sharing a line would serialise all heads' updates in one place.
+constexpr int kCounterStride = 64;
 void launch_attention(DType t, const AttnArgs &a, hipStream_t s, const LaunchEvents &ev = {});
 
 // u[m][c] = sum_i B[c][i] * x[m][i]   (x dtype, B fp32 [r][d])

@@ -643,7 +643,7 @@ __device__ __forceinline__ void merge_fold(float my_m, float my_l, const float (
     Mr = Mn;
 #pragma unroll
     for (int u = 0; u < NB; ++u) {
-        const float sc = __shfl(scl, u);  // zero for chunks past cn
+        const float sc = lane_f32(scl, u);  // zero for chunks past cn
 #pragma unroll
         for (int q = 0; q < PER; ++q) o[q] += ov[u][q] * sc;
     }
@@ -810,6 +810,13 @@ struct AttnTile {
         float rmax[4], rsum[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
+            if (r0 + j >= R) {  // no lane holds a row here (uniform): zero weights, nothing stored
+#pragma unroll
+                for (int t = 0; t < 4; ++t) S[t][j] = 0.f;
+                rmax[j] = -INFINITY;
+                rsum[j] = 0.f;
+                continue;
+            }
             const int r = r0 + 4 * lg + j;
             const int i = r / G;
             const int nvalid = r < R ? min(nk, len0 + i + 1 - kbase) : 0;
@@ -820,17 +827,15 @@ struct AttnTile {
                 S[t][j] = sv;
                 mx = fmaxf(mx, sv);
             }
-#pragma unroll
-            for (int o = 1; o < 16; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+            mx = row16_max(mx);
             float ps = 0.f;
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
-                const float pv = (mx == -INFINITY) ? 0.f : expf(S[t][j] - mx);
+                const float pv = (mx == -INFINITY) ? 0.f : exp_fast(S[t][j] - mx);
                 S[t][j] = pv;
                 ps += pv;
             }
-#pragma unroll
-            for (int o = 1; o < 16; o <<= 1) ps += __shfl_xor(ps, o);
+            ps = row16_sum(ps);
             rmax[j] = mx;
             rsum[j] = ps;
         }
@@ -967,12 +972,12 @@ __global__ void __launch_bounds__(64 * WPB, (ONE && T == DType::BF16) ? 3 : 1) a
     __syncthreads();
     if (threadIdx.x == 0) {
         const int nwg = (nch + WPB - 1) / WPB;
-        const int old = __hip_atomic_fetch_add(a.counters + b * a.n_kv + kvh, 1, __ATOMIC_RELEASE,
+        const int old = __hip_atomic_fetch_add(a.counters + (size_t)(b * a.n_kv + kvh) * kCounterStride, 1, __ATOMIC_RELEASE,
                                                __HIP_MEMORY_SCOPE_AGENT);
         is_last = (old == nwg - 1);
         if (is_last) {
             __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-            __hip_atomic_store(a.counters + b * a.n_kv + kvh, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(a.counters + (size_t)(b * a.n_kv + kvh) * kCounterStride, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
     }
     __syncthreads();
@@ -1056,19 +1061,17 @@ __global__ void __launch_bounds__(256) flash_prefill_kernel(AttnArgs a) {
                 S[t][j] = sv;
                 mx = fmaxf(mx, sv);
             }
-#pragma unroll
-            for (int o = 1; o < 16; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+            mx = row16_max(mx);
             const float mnew = fmaxf(m_run[j], mx);
-            const float alpha = mnew == -INFINITY ? 1.f : expf(m_run[j] - mnew);
+            const float alpha = mnew == -INFINITY ? 1.f : exp_fast(m_run[j] - mnew);
             float ps = 0.f;
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
-                const float pv = mnew == -INFINITY ? 0.f : expf(S[t][j] - mnew);
+                const float pv = mnew == -INFINITY ? 0.f : exp_fast(S[t][j] - mnew);
                 S[t][j] = pv;
                 ps += pv;
             }
-#pragma unroll
-            for (int o = 1; o < 16; o <<= 1) ps += __shfl_xor(ps, o);
+            ps = row16_sum(ps);
             l_run[j] = l_run[j] * alpha + ps;
             m_run[j] = mnew;
 #pragma unroll
