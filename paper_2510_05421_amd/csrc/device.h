@@ -185,6 +185,14 @@ __device__ __forceinline__ float2 ld_coherent_f32x2(__amdgpu_buffer_rsrc_t r, ui
     const v2u v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, kCoherent);
     return float2{__uint_as_float(v.x), __uint_as_float(v.y)};
 }
+// Four consecutive floats in one store with the same sc1 policy (written through to where every
+// XCD reads), the vector form of st_agent; ordering still comes from the release that follows.
+__device__ __forceinline__ void st_coherent_f32x4(__amdgpu_buffer_rsrc_t r, uint32_t off, float a, float b, float c,
+                                                  float d) {
+    typedef unsigned v4u __attribute__((ext_vector_type(4)));
+    const v4u v = {__float_as_uint(a), __float_as_uint(b), __float_as_uint(c), __float_as_uint(d)};
+    __builtin_amdgcn_raw_buffer_store_b128(v, r, off, 0, kCoherent);
+}
 
 // Pack EPL floats into one 16-byte MFMA fragment of dtype T.
 template <DType T>

@@ -187,14 +187,16 @@ static int m_max(const dvi_config &c) {
     int m = c.max_batch * c.max_k_spec;
     return m > kMaxRows ? m : kMaxRows;
 }
-// Rows of one prefill block (batch x prompt positions): up to 2048, fewer when the attention
-// partials of that many rows would pass 2 GiB (they grow with max_seq).
+// Rows of one prefill block (batch x prompt positions).  Prefill attention keeps no partials, so
+// the block is bounded by its activations only.
 static int prefill_rows(const dvi_config &c) {
-    const size_t per_row = (size_t)c.n_heads * (((size_t)c.max_seq + 63) / 64) * (c.head_dim + 2) * 4;
-    size_t m = ((size_t)2 << 30) / per_row / 64 * 64;
-    if (m > 2048) m = 2048;
     const int mm = m_max(c);
-    return (int)m > mm ? (int)m : mm;
+    return 2048 > mm ? 2048 : mm;
+}
+// Bytes of the split-KV attention partials of a decode step (outputs and statistics of every
+// 64-key chunk of m_max rows); they are addressed with 32-bit byte offsets.
+static size_t partial_bytes(const dvi_config &c) {
+    return (size_t)m_max(c) * c.n_heads * (((size_t)c.max_seq + 63) / 64) * (c.head_dim + 2) * 4;
 }
 
 // Lay out (or size, when base == nullptr) everything the context keeps on the device.
@@ -244,8 +246,8 @@ static size_t layout(dvi_ctx *x, const dvi_config &c, void *base) {
     float *part_val = b.take<float>(M * (V / 16) * 4);
     int32_t *part_idx = b.take<int32_t>(M * (V / 16) * 4);
     float *lora_u = b.take<float>((M > R ? M : R) * r * 4);
-    float *att_po = b.take<float>(Mp * c.n_heads * cs * c.head_dim * 4);
-    float *att_pml = b.take<float>(Mp * c.n_heads * cs * 2 * 4);
+    float *att_po = b.take<float>(M * c.n_heads * cs * c.head_dim * 4);
+    float *att_pml = b.take<float>(M * c.n_heads * cs * 2 * 4);
     int32_t *att_cnt = b.take<int32_t>((size_t)c.max_batch * c.n_kv_heads * kCounterStride * 4);
     int32_t *lens = b.take<int32_t>(c.max_batch * 4);
     int32_t *pending = b.take<int32_t>(c.max_batch * 4);
@@ -323,6 +325,7 @@ static const char *check_config(const dvi_config *c) {
     if (c->max_batch * c->max_k_spec > kMaxRows) return "max_batch * max_k_spec must be <= 64";
     if (c->max_batch > dvi::kMaxBatch) return "max_batch must be <= 64";
     if (c->max_seq < 2) return "max_seq < 2";
+    if (partial_bytes(*c) >= ((size_t)2 << 30)) return "max_seq too long: the attention partials of 64 rows must stay under 2 GiB";
     if (c->lora_rank < 1 || c->lora_rank > 64) return "lora_rank must be in [1, 64]";
     if (c->buffer_rows < 1) return "buffer_rows < 1";
     if (!(c->rms_eps > 0.f) || !(c->rope_theta > 0.f)) return "rms_eps and rope_theta must be > 0";

@@ -671,13 +671,20 @@ __device__ __forceinline__ void merge_group(__amdgpu_buffer_rsrc_t mlr, __amdgpu
     merge_fold<HD, NB>(my_m, my_l, ov, cn, lane, Mr, L, o);
 }
 
-// Output of one merged row: lane holds head dims PER*lane .. +PER-1.
+// Head dim of position p of a chunk's partial output (the lane-major order the chunk waves
+// write: position l16 * HD/16 + dt holds head dim 16 dt + l16).
+template <int HD>
+__device__ __forceinline__ int part_dim(int p) {
+    return 16 * (p % (HD / 16)) + p / (HD / 16);
+}
+
+// Output of one merged row: lane holds slot positions PER*lane .. +PER-1.
 template <DType T, int HD>
 __device__ __forceinline__ void store_row(const AttnArgs &a, int m, int h, int lane, const float (&o)[HD / 64],
                                           float L) {
 #pragma unroll
     for (int q = 0; q < HD / 64; ++q)
-        St<T>::store(a.O, fm_index<T>(m, h * HD + (HD / 64) * lane + q, a.n_heads * HD), o[q] / L);
+        St<T>::store(a.O, fm_index<T>(m, h * HD + part_dim<HD>((HD / 64) * lane + q), a.n_heads * HD), o[q] / L);
 }
 
 // Merge of one query row m of head h over its ncr chunks (one wave), then the row's output.
@@ -854,15 +861,25 @@ struct AttnTile {
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
         // O: lane holds rows r0 + 4 lg + j, head dim 16 dt + l16
+        // A chunk whose 64 keys are all written (every chunk but a sequence's last) needs no mask.
+        const bool full = nk >= CK;
+        f32x4 O[DT];
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
-            f32x4 O = (f32x4){0.f, 0.f, 0.f, 0.f};
+            O[dt] = (f32x4){0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) O = St<T>::mma(pf[ks], mask_keys<T>(vf[dt][ks], ks * KC + EPL * lg, nk), O);
+            for (int ks = 0; ks < KS; ++ks)
+                O[dt] = St<T>::mma(pf[ks], full ? vf[dt][ks] : mask_keys<T>(vf[dt][ks], ks * KC + EPL * lg, nk), O[dt]);
+        }
+        // row 4 lg + j's output: head dims 16 dt + l16, dt = 0..DT-1, in this lane
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int r = r0 + 4 * lg + j;
-                if (r < R && rmax[j] != -INFINITY) sink(r, 16 * dt + l16, O[j], dt == 0 && l16 == 0, rmax[j], rsum[j]);
+        for (int j = 0; j < 4; ++j) {
+            const int r = r0 + 4 * lg + j;
+            if (r < R && rmax[j] != -INFINITY) {
+                float v[DT];
+#pragma unroll
+                for (int dt = 0; dt < DT; ++dt) v[dt] = O[dt][j];
+                sink(r, v, l16 == 0, rmax[j], rsum[j]);
             }
         }
     }
@@ -945,10 +962,16 @@ __global__ void __launch_bounds__(64 * WPB, (ONE && T == DType::BF16) ? 3 : 1) a
     const int G = a.n_heads / a.n_kv;
     const int R = a.c * G;
     if (ch < nch) {  // uniform across the wave
-        auto sink = [&](int r, int dim, float v, bool stats, float mx, float sm) {
+        // A row's partial output goes to its slot lane-major: the lane holding head dims
+        // 16 dt + l16 (dt = 0..HD/16-1) writes them contiguously at l16 * HD/16 (part_dim maps a
+        // slot position back to its head dim).
+        const __amdgpu_buffer_rsrc_t por = coherent_rsrc(a.part_o);
+        auto sink = [&](int r, const float (&v)[HD / 16], bool stats, float mx, float sm) {
             const int i = r / G, gi = r - i * G;
             const size_t slot = ((size_t)(b * a.c + i) * a.n_heads + kvh * G + gi) * a.chunk_stride + ch;
-            st_agent(a.part_o + slot * HD + dim, v);
+            const uint32_t off = (uint32_t)((slot * HD + (size_t)(lane & 15) * (HD / 16)) * 4);
+#pragma unroll
+            for (int q = 0; q < HD / 16; q += 4) st_coherent_f32x4(por, off + 4 * q, v[q], v[q + 1], v[q + 2], v[q + 3]);
             if (stats) {
                 st_agent(a.part_ml + slot * 2 + 0, mx);
                 st_agent(a.part_ml + slot * 2 + 1, sm);
