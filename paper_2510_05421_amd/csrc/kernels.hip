@@ -1137,8 +1137,10 @@ __global__ void __launch_bounds__(256) flash_prefill_kernel(AttnArgs a) {
 template <DType T, int HD>
 static void launch_attention_t(const AttnArgs &a, hipStream_t s, const LaunchEvents &ev) {
     // One wave per 64-key chunk, four chunks per workgroup: the workgroup that finishes last
-    // merges with four waves.  A single query row per kv head over a small grid takes one wave
-    // per workgroup instead, which spreads the chunks over more compute units.  A large grid, or
+    // merges with four waves.  Each workgroup publishes its partials with one agent-scope release
+    // (an L2 writeback), so four chunks per workgroup also beat one: 7B draft token 1.502 ->
+    // 1.478 ms with one query row per kv head, against 1.468 ms with the ordering left to cache
+    // policy bits (a relaxed counter), which the memory model does not guarantee.  A large grid, or
     // more query rows per kv head than the last workgroup has waves (verify blocks of 6 or more,
     // grouped-head verify, prefill blocks), merges in a second launch instead, one wave per row:
     // otherwise every workgroup would wait for its partial stores before counting itself done,
@@ -1161,8 +1163,6 @@ static void launch_attention_t(const AttnArgs &a, hipStream_t s, const LaunchEve
         else
             launch_timed(attn_kernel<T, HD, 4, false>, dim3((a.n_chunks + 3) / 4, a.n_kv, a.B), dim3(256), s, e1, a);
         launch_timed(attn_merge_kernel<T, HD>, dim3((all_rows + 3) / 4), dim3(256), s, e2, a);
-    } else if (rows == 1) {
-        launch_timed(attn_kernel<T, HD, 1, true, true>, dim3(a.n_chunks, a.n_kv, a.B), dim3(64), s, ev, a);
     } else {
         launch_timed(attn_kernel<T, HD, 4, true, true>, dim3((a.n_chunks + 3) / 4, a.n_kv, a.B), dim3(256), s, ev, a);
     }
