@@ -55,6 +55,7 @@ struct Scratch {
     int chunk_stride = 0;
     float *part_val = nullptr;
     int32_t *part_idx = nullptr;
+    float *kpart = nullptr;  // split decode GEMMs' partial tiles (null: one-launch reduction)
 };
 
 }  // namespace
@@ -249,6 +250,16 @@ static size_t layout(dvi_ctx *x, const dvi_config &c, void *base) {
     float *att_po = b.take<float>(M * c.n_heads * cs * c.head_dim * 4);
     float *att_pml = b.take<float>(M * c.n_heads * cs * 2 * 4);
     int32_t *att_cnt = b.take<int32_t>((size_t)c.max_batch * c.n_kv_heads * kCounterStride * 4);
+    // partial tiles of the decode GEMMs that split their K pieces over workgroups (33-64 rows)
+    size_t kpart_bytes = 0;
+    if (c.max_batch * c.max_k_spec > 32 || c.max_batch > 32) {
+        const DType dt = c.dtype == DVI_BF16 ? DType::BF16 : DType::F32;
+        const size_t sz[] = {gemm_split_bytes(dt, qkv_rows(c), (int)d), gemm_split_bytes(dt, (int)d, (int)qd),
+                             gemm_split_bytes(dt, (int)(2 * F), (int)d), gemm_split_bytes(dt, (int)d, (int)F),
+                             gemm_split_bytes(dt, (int)V, (int)d)};
+        for (size_t z : sz) kpart_bytes = z > kpart_bytes ? z : kpart_bytes;
+    }
+    float *kpart = kpart_bytes ? b.take<float>(kpart_bytes) : nullptr;
     int32_t *lens = b.take<int32_t>(c.max_batch * 4);
     int32_t *pending = b.take<int32_t>(c.max_batch * 4);
     int32_t *drafts = b.take<int32_t>(Bk * 4);
@@ -293,6 +304,7 @@ static size_t layout(dvi_ctx *x, const dvi_config &c, void *base) {
         x->lora_u = lora_u;
         x->ws_scr.att_po = att_po; x->ws_scr.att_pml = att_pml; x->ws_scr.att_cnt = att_cnt;
         x->ws_scr.chunk_stride = (int)cs; x->ws_scr.part_val = part_val; x->ws_scr.part_idx = part_idx;
+        x->ws_scr.kpart = kpart;
         x->scr = x->ws_scr;
         x->chunk_stride = (int)cs;
         x->lens = lens; x->pending = pending; x->drafts = drafts; x->targets = targets; x->forced = forced;
@@ -542,6 +554,7 @@ static void gemm(dvi_ctx *x, Epi e, int cls, const void *W, const void *X, int M
     a.N = N;
     a.K = K;
     a.sinv_rows = x->sinv_rows;
+    a.kpart = x->scr.kpart;
     const LaunchEvents ev = probe_begin(x, cls);
     if (!launch_gemm(x->dt, e, a, x->stream, ev))
         (void)fail(x, DVI_ERR_DEVICE, "no GEMM variant for %d rows of epilogue %d", M, (int)e);

@@ -102,6 +102,11 @@ struct GemmArgs {
     uint64_t seed;
     const int32_t *rng_step;
     int rng_row0, rng_row_stride;
+    // Decode GEMM at 33-64 tokens: when set, the K pieces run in separate workgroups that write
+    // their partial tiles here (gemm_split_bytes(N, K) bytes), then a second launch adds them in
+    // order and runs the epilogue; when null, one launch reduces each tile's pieces itself.
+    // Either way every output gets the same arithmetic.
+    float *kpart;
 };
 // Optional start/stop events for one launch: when set, the kernel is launched with
 // hipExtLaunchKernelGGL, which stamps the events at the kernel's own start and end (the same
@@ -114,6 +119,8 @@ struct LaunchEvents {
 // GEMM, which needs sinv_rows when ss_in is set and takes every epilogue but EPI_LOGITS
 // (returns false).  Each kernel's arithmetic per output is independent of M.
 bool launch_gemm(DType t, Epi e, const GemmArgs &a, hipStream_t s, const LaunchEvents &ev = {});
+// Bytes of GemmArgs::kpart for an N x K matrix (64 tokens); 0 when that matrix never splits.
+size_t gemm_split_bytes(DType t, int N, int K);
 
 // Row m = b*c + i: h = E[tok[b*tok_stride + i]] (fp32, row stride ldh), its per-16-column
 // sums of squares (ss, stride ld_ss) and dtype(h * g) (hg, FM, row m).

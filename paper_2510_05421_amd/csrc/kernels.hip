@@ -176,6 +176,108 @@ __global__ void __launch_bounds__(64 * WMAX) gemm_kernel(GemmArgs a) {
 }
 
 // ------------------------------------------------------------------------------------------
+// Decode GEMM at 33-64 tokens with the K pieces spread over workgroups.  Each output gets exactly
+// gemm_kernel's arithmetic: K cut into the same w pieces (w from (N, K)), each piece accumulated
+// from zero in the tile's rotated chunk order, the pieces added in order 0..w-1, then the same
+// epilogue.  Only the placement differs.  Workgroup (tile group g, piece p) of 16 waves takes
+// piece p of 16 consecutive tiles, one per wave, and loads piece p's activation fragments (every
+// token group: 4 KiB per chunk at 64 tokens) into LDS once for all 16 waves; gemm_kernel instead
+// has every workgroup read the activations of all its pieces for its 1-3 tiles, which at 64
+// tokens crosses from L2 4x the weight bytes (out-proj, down).  Each wave writes its partial tile;
+// gemm_fold_kernel adds the pieces in order and runs the epilogue.  Workgroup id = g * w + p, so
+// with w = 16 the workgroups of one piece share an XCD and its L2 copy of the piece.
+// ------------------------------------------------------------------------------------------
+constexpr int kSplitTiles = 16;   // tiles (one per wave) of a split workgroup
+constexpr int kSplitXPer = 8;     // activation fragments per wave: at most 128 per piece (128 KiB LDS)
+
+template <DType T, int MG>
+__global__ void __launch_bounds__(64 * kSplitTiles) gemm_split_kernel(GemmArgs a, int w) {
+    extern __shared__ uint4 xs[];  // fragment (chunk c - c0, group g) at (c - c0) * MG + g, 64 lanes each
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int p = blockIdx.x % w, nt = (blockIdx.x / w) * kSplitTiles + wave;
+    const bool tv = nt < a.N / 16;  // uniform across the wave
+    const int KT = a.K / ((T == DType::BF16) ? 32 : 16);
+    const int c0 = (p * KT) / w, c1 = ((p + 1) * KT) / w, nc = c1 - c0;
+    const uint4 zero = {0u, 0u, 0u, 0u};
+    // the piece's activation fragments, all requested before the first weight load; rows past M
+    // are zero (as gemm_kernel's lanes that load nothing)
+    const int nfrag = nc * MG;
+    uint4 xr[kSplitXPer];
+#pragma unroll
+    for (int q = 0; q < kSplitXPer; ++q) {
+        const int f = wave + kSplitTiles * q, c = f / MG, g = f - c * MG;
+        xr[q] = (f < nfrag && 16 * g + (lane & 15) < a.M)
+                    ? ld_stream((const uint4 *)a.X + ((size_t)g * KT + c0 + c) * 64 + lane)
+                    : zero;
+    }
+    // the tile's weights through a ring of S chunk steps, in the rotated order
+    const int rot = (nt / 12) % nc;
+    const uint4 *wp = (const uint4 *)a.W + (size_t)nt * KT * 64 + lane;
+    constexpr int S = 4;
+    uint4 wr[S];
+    auto wfetch = [&](int st) {
+        int c = st + rot;
+        if (c >= nc) c -= nc;
+        return (tv && st < nc) ? ld_stream(wp + (size_t)(c0 + c) * 64) : zero;
+    };
+#pragma unroll
+    for (int st = 0; st < S; ++st) wr[st] = wfetch(st);
+#pragma unroll
+    for (int q = 0; q < kSplitXPer; ++q) {
+        const int f = wave + kSplitTiles * q;
+        if (f < nfrag) xs[f * 64 + lane] = xr[q];
+    }
+    __syncthreads();
+    f32x4 acc[MG];
+#pragma unroll
+    for (int g = 0; g < MG; ++g) acc[g] = (f32x4){0.f, 0.f, 0.f, 0.f};
+    for (int s0 = 0; s0 < nc; s0 += S) {
+#pragma unroll
+        for (int st = 0; st < S; ++st) {
+            if (s0 + st < nc) {  // uniform
+                int c = s0 + st + rot;
+                if (c >= nc) c -= nc;
+#pragma unroll
+                for (int g = 0; g < MG; ++g) acc[g] = St<T>::mma(wr[st], xs[(c * MG + g) * 64 + lane], acc[g]);
+            }
+            wr[st] = wfetch(s0 + st + S);
+        }
+    }
+    if (!tv) return;
+    f32x4 *dst = (f32x4 *)a.kpart + ((size_t)nt * w + p) * MG * 64 + lane;
+#pragma unroll
+    for (int g = 0; g < MG; ++g) dst[g * 64] = acc[g];
+}
+
+// The pieces of each tile added in order 0..W-1 (P0 + P1, then + P2, ...: gemm_kernel's
+// wave-order sum), then the tile's epilogue.  Workgroup nt holds tile nt, wave g its token group g
+// (the epilogue treats token groups independently); 1/rms of every token as gemm_kernel computes
+// it for more than 32 tokens.  All W pieces of a group are requested before the first add.
+template <DType T, int EPI, int W>
+__global__ void __launch_bounds__(256) gemm_fold_kernel(GemmArgs a, int mg) {
+    __shared__ float sinv[64];
+    const int lane = threadIdx.x & 63, g = threadIdx.x >> 6, nt = blockIdx.x;
+    if (a.ss_in != nullptr)
+        for (int m = g; m < a.M; m += 4) {
+            const float v = inv_rms(a.ss_in + (size_t)m * a.ld_ss_in, a.K / 16, a.K, a.eps);
+            if (lane == 0) sinv[m] = v;
+        }
+    __syncthreads();
+    if (g >= mg) return;  // uniform across the wave
+    EpiOperands<1> pre;
+    epilogue_prefetch<1, EPI>(a, nt, pre, 16 * g);
+    const f32x4 *src = (const f32x4 *)a.kpart + ((size_t)nt * W * mg + g) * 64 + lane;
+    f32x4 v[W];
+#pragma unroll
+    for (int p = 0; p < W; ++p) v[p] = src[(size_t)p * mg * 64];
+    f32x4 mine[1] = {v[0]};
+#pragma unroll
+    for (int p = 1; p < W; ++p) mine[0] = mine[0] + v[p];
+    epilogue_prefetch_rope<1, EPI>(a, nt, pre);
+    gemm_epilogue<T, 1, EPI>(a, nt, mine, sinv + 16 * g, pre, 16 * g);
+}
+
+// ------------------------------------------------------------------------------------------
 // Large-M GEMM (the prefill: M = batch x prompt block, up to a few thousand tokens; the drafter
 // update's replay rows).  1/rms of each token comes from rms_rows_kernel; the epilogue is the
 // decode GEMM's, per tile, at the wave's token offset.
@@ -389,6 +491,15 @@ static void launch_timed(void (*kernel)(Arg), dim3 grid, dim3 block, hipStream_t
     else
         kernel<<<grid, block, 0, s>>>(a);
 }
+// the same with a second argument and dynamic LDS
+template <typename Arg, typename Arg2>
+static void launch_timed(void (*kernel)(Arg, Arg2), dim3 grid, dim3 block, hipStream_t s, const LaunchEvents &ev,
+                         const Arg &a, Arg2 b, size_t lds) {
+    if (ev.start || ev.stop)
+        hipExtLaunchKernelGGL(kernel, grid, block, lds, s, ev.start, ev.stop, 0, a, b);
+    else
+        kernel<<<grid, block, lds, s>>>(a, b);
+}
 
 template <DType T, int EPI, int RT, int WMAX>
 static void gemm_dispatch_mg(const GemmArgs &a, dim3 grid, dim3 block, hipStream_t s, const LaunchEvents &ev) {
@@ -427,6 +538,48 @@ static void gemm_dispatch(Epi e, const GemmArgs &a, GemmShape sh, hipStream_t s,
     }
 }
 
+// The split launch applies to matrices of 16 K pieces (one tile per 16-wave workgroup in
+// gemm_kernel, whose activation reads at 64 tokens are 4x the weight bytes) whose piece of 64
+// tokens' activations fits the LDS of one split workgroup.  In the 7B batch-8 verify (64 rows)
+// out-proj and down went from 21.7 + 47.3 us to 47 us for both, split and fold launches
+// included.  Matrices of 8 pieces keep gemm_kernel, whose three tiles per workgroup read the
+// activations 1.3x the weight bytes: there the partial tiles' round trip through memory costs
+// more than it saves (gate/up 59 -> 71 us, QKV 40 -> 55 us, head 75 -> 95 us).
+static bool split_fits(const GemmShape &sh, int K, int KC, int mg) {
+    const int KT = K / KC, ncmax = (KT + sh.waves - 1) / sh.waves;
+    return sh.waves == 16 && ncmax * mg <= kSplitTiles * kSplitXPer;
+}
+
+size_t gemm_split_bytes(DType t, int N, int K) {
+    const GemmShape sh = gemm_shape(N, K, pack_kc(t), 64);
+    if (!split_fits(sh, K, pack_kc(t), 4)) return 0;
+    return (size_t)(N / 16) * sh.waves * 4 * 1024;
+}
+
+template <DType T, int EPI>
+static void launch_split(const GemmArgs &a, const GemmShape &sh, hipStream_t s, const LaunchEvents &ev) {
+    const int NT = a.N / 16, mg = (a.M + 15) / 16, KT = a.K / pack_kc(T);
+    const int ncmax = (KT + sh.waves - 1) / sh.waves;
+    LaunchEvents e1 = ev, e2 = ev;  // one interval around both launches
+    e1.stop = nullptr;
+    e2.start = nullptr;
+    const dim3 g1((NT + kSplitTiles - 1) / kSplitTiles * sh.waves), b1(64 * kSplitTiles);
+    const size_t lds = (size_t)ncmax * mg * 1024;
+    if (mg == 3) launch_timed(gemm_split_kernel<T, 3>, g1, b1, s, e1, a, sh.waves, lds);
+    else launch_timed(gemm_split_kernel<T, 4>, g1, b1, s, e1, a, sh.waves, lds);
+    launch_timed(gemm_fold_kernel<T, EPI, 16>, dim3(NT), dim3(256), s, e2, a, mg, 0);
+}
+
+template <DType T>
+static void launch_split_epi(Epi e, const GemmArgs &a, const GemmShape &sh, hipStream_t s, const LaunchEvents &ev) {
+    switch (e) {
+        case EPI_RESID: launch_split<T, EPI_RESID>(a, sh, s, ev); break;
+        case EPI_QKV: launch_split<T, EPI_QKV>(a, sh, s, ev); break;
+        case EPI_SWIGLU: launch_split<T, EPI_SWIGLU>(a, sh, s, ev); break;
+        default: launch_split<T, EPI_LOGITS>(a, sh, s, ev); break;
+    }
+}
+
 bool launch_gemm(DType t, Epi e, const GemmArgs &a, hipStream_t s, const LaunchEvents &ev) {
     if (a.M > 64 || a.large_m) {
         if (e == EPI_LOGITS) return false;
@@ -437,6 +590,13 @@ bool launch_gemm(DType t, Epi e, const GemmArgs &a, hipStream_t s, const LaunchE
         return true;
     }
     const GemmShape sh = gemm_shape(a.N, a.K, pack_kc(t), a.M);
+    if (a.kpart != nullptr && a.M > 32 && split_fits(sh, a.K, pack_kc(t), (a.M + 15) / 16)) {
+        if (t == DType::BF16)
+            launch_split_epi<DType::BF16>(e, a, sh, s, ev);
+        else
+            launch_split_epi<DType::F32>(e, a, sh, s, ev);
+        return true;
+    }
     if (t == DType::BF16)
         gemm_dispatch<DType::BF16>(e, a, sh, s, ev);
     else

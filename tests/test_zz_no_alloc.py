@@ -2,8 +2,10 @@
 
 Both run the same kernels on the same drafted state; dvi_verify_static only keeps the attention
 partials, merge counters and argmax partials in the library's static device array instead of the
-workspace.  Its targets, accept lengths and logits must equal dvi_verify's bit for bit, on two calls
-in a row (the second with fewer rows), and a verify that would need more than the array's size is
+workspace, and at 33-64 rows it reduces each GEMM tile's K pieces inside one launch where
+dvi_verify spreads them over workgroups and adds them in a second launch (same order, same bits).
+Its targets, accept lengths and logits must equal dvi_verify's bit for bit, on two calls in a row
+(the second with fewer rows), and a verify that would need more than the array's size is
 refused."""
 import numpy as np
 import pytest
@@ -39,23 +41,27 @@ def _both(eng, k, forced):
     return (tg1, m1, lg1), (tg2, m2, lg2)
 
 
-@pytest.mark.parametrize("name", ["tiny", "7b_L4"])
-def test_verify_static_equals_verify(name):
+@pytest.mark.parametrize("name,B,k", [("tiny", 3, 6), ("7b_L4", 3, 6), ("tiny", 6, 8), ("7b_L4", 6, 8),
+                                      ("tiny", 8, 8), ("7b_L4", 8, 8)])
+def test_verify_static_equals_verify(name, B, k):
+    """18 rows (one-launch GEMMs on both sides), 48 and 64 rows (dvi_verify splits its GEMMs)."""
     shape = gu.SHAPES[name]
-    B, P, k = 3, 70, 6
+    P = 70
     prompts = synth.make_prompts(shape.vocab, B, P, 41)
     _say("verify_static %s B=%d P=%d k=%d then k=2" % (name, B, P, k))
-    eng, _ = gu.engine(shape, max_batch=B, max_seq=P + 40)
+    eng, _ = gu.engine(shape, max_batch=B, max_seq=P + 40, max_k_spec=k)
     ar, _ = eng.generate(prompts, 20, 1)
     eng.prefill(prompts)
-    # first call: drafts = greedy continuation with one wrong position per sequence (m = 0, 2, 6)
+    # first call: drafts = greedy continuation with one wrong position per sequence (none for
+    # the sequences whose wrong position is k)
+    wrong = [(0, 2, k, 1, 3, 5, k, 4)[b] for b in range(B)]
     forced = ar[:, 1:1 + k].copy()
-    for b, j in enumerate((0, 2, k)):
+    for b, j in enumerate(wrong):
         if j < k:
             forced[b, j] = (forced[b, j] + 1) % shape.vocab
     (tg1, m1, lg1), (tg2, m2, lg2) = _both(eng, k, forced)
     assert np.array_equal(tg1, tg2) and np.array_equal(m1, m2) and np.array_equal(lg1, lg2)
-    assert list(m2) == [0, 2, k]
+    assert list(m2) == wrong
     tok, n, m = eng.commit()
     # second call, fewer rows (k = 2), from the committed state
     forced2 = np.stack([ar[b, 1 + n[b]:3 + n[b]] for b in range(B)]).astype(np.int32)
