@@ -52,22 +52,43 @@ def kernel_sources_sha256():
     return h.hexdigest()
 
 
-def measured_traffic(probe, workload, k_spec):
-    """Bytes per launch from the committed counter summary, or None when there is none for
-    this kernel and workload or the kernel source has changed since it was taken."""
-    rel = TRAFFIC_PROFILES.get(probe)
+def profile_fields(rel):
+    """The `- `key`: `value`` fields of a committed counter summary, or {} when it is missing or
+    was taken on other kernel sources than the current ones."""
     if rel is None or not os.path.exists(os.path.join(ROOT, rel)):
-        return None
+        return {}
     fields = {}
     with open(os.path.join(ROOT, rel)) as f:
         for line in f:
             if line.startswith("- `") and "`: " in line:
                 key, val = line[3:].split("`: ", 1)
                 fields[key] = val.strip().strip("`")
-    if (fields.get("kernel_sources_sha256") != kernel_sources_sha256() or fields.get("workload") != workload
-            or fields.get("k_spec") != str(k_spec)):
+    return fields if fields.get("kernel_sources_sha256") == kernel_sources_sha256() else {}
+
+
+def measured_traffic(probe, workload, k_spec):
+    """Bytes per launch from the committed counter summary, or None when there is none for
+    this kernel and workload or the kernel source has changed since it was taken."""
+    fields = profile_fields(TRAFFIC_PROFILES.get(probe))
+    if fields.get("workload") != workload or fields.get("k_spec") != str(k_spec):
         return None
     return int(float(fields["traffic_bytes_per_launch"]))
+
+
+# MFMA counters of the drafter update's forward GEMM over a full replay ring: the committed
+# summary of a rocprofv3 --pmc pass (SQ_INSTS_VALU_MFMA_MOPS_BF16, SQ_VALU_MFMA_BUSY_CYCLES,
+# GRBM_GUI_ACTIVE) over this benchmark's 13B workload.
+MFMA_PROFILE = "profiles/drafter_update_13b.md"
+
+
+def measured_mfma(workload):
+    fields = profile_fields(MFMA_PROFILE)
+    if fields.get("workload") != workload:
+        return None
+    return {"forward_gemm_counter_gflop": float(fields["forward_gemm_counter_gflop"]),
+            "forward_gemm_counter_tflop_s": float(fields["forward_gemm_counter_tflop_s"]),
+            "forward_gemm_mfma_busy_frac": float(fields["forward_gemm_mfma_busy_frac"]),
+            "source": MFMA_PROFILE}
 
 
 def log(msg):
@@ -270,7 +291,9 @@ def main():
         peak = 2500.0 if shape.bf16 else 157.3
         upd_full = {"rows": R, "ms": round(u_ms, 4), "gflop": round(flops / 1e9, 2),
                     "tflop_s": round(flops / (u_ms * 1e-3) / 1e12, 2), "mfma_peak_tflop_s": peak,
-                    "frac": round(flops / (u_ms * 1e-3) / 1e12 / peak, 4), "forward_gemm_gflop": round(gemm_flops / 1e9, 2)}
+                    "frac": round(flops / (u_ms * 1e-3) / 1e12 / peak, 4), "forward_gemm_gflop": round(gemm_flops / 1e9, 2),
+                    # matrix-unit utilisation of the forward GEMM read from rocprofv3 counters
+                    "mfma_counters": measured_mfma(wl.name)}
         log("drafter update over a full %d-row ring: %.3f ms, %.1f GFLOP -> %.1f TFLOP/s (%.3f of %g)"
             % (R, u_ms, flops / 1e9, upd_full["tflop_s"], upd_full["frac"], peak))
 
