@@ -87,6 +87,7 @@ def measured_mfma(workload):
         return None
     return {"forward_gemm_counter_gflop": float(fields["forward_gemm_counter_gflop"]),
             "forward_gemm_counter_tflop_s": float(fields["forward_gemm_counter_tflop_s"]),
+            "forward_gemm_mfma_frac_of_peak": float(fields["forward_gemm_mfma_frac_of_peak"]),
             "forward_gemm_mfma_busy_frac": float(fields["forward_gemm_mfma_busy_frac"]),
             "source": MFMA_PROFILE}
 
