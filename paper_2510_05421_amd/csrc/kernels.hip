@@ -1522,18 +1522,29 @@ void launch_ring_copy(const int32_t *cl, int max_rows, const void *hk_hat, int d
 // these kernels turn them into the loss gradient and the LoRA-factor gradients.
 // ------------------------------------------------------------------------------------------
 // stats[0] = n rows, [1] = accepted rows, [2] = fresh rows, [3] = fresh accepted rows.
+// Row counts of the ring (all, accepted, fresh, fresh and accepted): one wave, lane-strided, the
+// integer sums reduced across the wave (exact in any order).
 __global__ void upd_counts_kernel(const int8_t *r, const int8_t *fresh, int n, float *stats) {
-    if (threadIdx.x != 0) return;
+    const int lane = threadIdx.x & 63;
     int na = 0, nf = 0, nfa = 0;
-    for (int i = 0; i < n; ++i) {
-        na += r[i] != 0;
-        nf += fresh[i] != 0;
-        nfa += (r[i] != 0) && (fresh[i] != 0);
+    for (int i = lane; i < n; i += 64) {
+        const bool acc = r[i] != 0, fr = fresh[i] != 0;
+        na += acc;
+        nf += fr;
+        nfa += acc && fr;
     }
-    stats[0] = (float)n;
-    stats[1] = (float)na;
-    stats[2] = (float)nf;
-    stats[3] = (float)nfa;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        na += __shfl_xor(na, o);
+        nf += __shfl_xor(nf, o);
+        nfa += __shfl_xor(nfa, o);
+    }
+    if (lane == 0) {
+        stats[0] = (float)n;
+        stats[1] = (float)na;
+        stats[2] = (float)nf;
+        stats[3] = (float)nfa;
+    }
 }
 
 // Row i: p = softmax(z), q = softmax(l/tau); KL, entropy, log p(a); then overwrite z with
@@ -1621,10 +1632,12 @@ __global__ void __launch_bounds__(1024) upd_rows_kernel(UpdateArgs u, const floa
     }
 }
 
+// The loss and its terms, summed over the ring rows: one wave, lane l adding rows l, l + 64, ...
+// in order, then the fixed wave tree.
 __global__ void upd_loss_kernel(UpdateArgs u, const float *counts) {
-    if (threadIdx.x != 0) return;
+    const int lane = threadIdx.x & 63;
     float loss = 0.f, kl = 0.f, ent = 0.f, ce = 0.f, pg = 0.f;
-    for (int i = 0; i < u.n; ++i) {
+    for (int i = lane; i < u.n; i += 64) {
         const float *st = u.row_stats + (size_t)i * 8;
         loss += st[3];
         kl += st[0];
@@ -1632,6 +1645,12 @@ __global__ void upd_loss_kernel(UpdateArgs u, const float *counts) {
         ce -= (float)u.r[i] * st[2];
         pg -= ((float)u.r[i] - u.baseline) * (float)u.fresh[i] * st[2];
     }
+    loss = wave_sum(loss);
+    kl = wave_sum(kl);
+    ent = wave_sum(ent);
+    ce = wave_sum(ce);
+    pg = wave_sum(pg);
+    if (lane != 0) return;
     u.loss_out[0] = loss;
     u.loss_out[1] = kl / counts[0];
     u.loss_out[2] = ce / fmaxf(counts[1], 1.f);
