@@ -54,6 +54,7 @@ def test_workspace_size_covers_weights_and_cache():
 @pytest.mark.parametrize("bad", [
     dict(d_model=100), dict(head_dim=96), dict(n_kv_heads=3), dict(vocab=4001), dict(max_k_spec=17),
     dict(max_batch=9, max_k_spec=8), dict(lora_rank=0), dict(split_k=0), dict(split_k=99),
+    dict(max_seq=10_000_000),   # attention partials of 64 rows past 2 GiB (32-bit offsets)
 ])
 def test_invalid_configs_are_rejected_on_the_host(bad):
     from paper_2510_05421_amd.engine import workspace_bytes

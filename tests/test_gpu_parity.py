@@ -423,6 +423,25 @@ def test_argmax_ties_go_to_the_lowest_id(name, kind):
         eng.close()
 
 
+def test_measure_read_rate():
+    """The streaming-read reference the benchmark reports beside the nominal peak: a 512 MiB buffer
+    (past the 256 MB last-level cache) reads at a plausible HBM rate, below the 8 TB/s nominal
+    peak; arguments it cannot use are refused."""
+    import ctypes
+    import torch
+    from paper_2510_05421_amd._abi import ERR_ARG
+    eng, _ = gu.engine(gu.SHAPES["tiny"], max_seq=64)
+    rate = eng.read_rate(512 << 20, reps=3)
+    _say("streaming read: %.0f GB/s" % rate)
+    assert 1000.0 < rate < 8000.0
+    buf = torch.empty(4 << 20, dtype=torch.uint8, device=eng.device)
+    v = ctypes.c_double()
+    for nbytes, reps in ((1000, 3), ((1 << 20) + 8, 3), (4 << 20, 0)):
+        assert eng.status_of("dvi_measure_read_rate", buf.data_ptr(), nbytes, reps, ctypes.byref(v)) == ERR_ARG
+    del buf
+    eng.close()
+
+
 def test_run_to_run_determinism():
     shape = gu.SHAPES["1b_L4"]
     prompt = synth.make_prompts(shape.vocab, 1, 50, 4)
