@@ -287,7 +287,7 @@ static size_t layout(dvi_ctx *x, const dvi_config &c, void *base) {
     float *upd_stats = b.take<float>(R * 8 * 4);
     float *upd_dA = b.take<float>(V * r * 4);
     float *upd_du = b.take<float>(R * r * 4);
-    float *upd_dup = b.take<float>(R * kDuSlices * r * 4);
+    float *upd_dup = b.take<float>(R * grad_parts((int)V) * 16 * 4);
     float *upd_dB = b.take<float>(r * d * 4);
     float *upd_loss = b.take<float>(16 * 4);
     float *mA = b.take<float>(V * r * 4);

@@ -208,7 +208,8 @@ void launch_ring_copy(const int32_t *copy_list, int max_rows, const void *hk_hat
                       const float *vlogits, int V, void *ring_h, float *ring_logits, hipStream_t s);
 
 // ---- drafter update (Section 3.4) ----
-constexpr int kDuSlices = 8;  // vocabulary slices of the du reduction
+constexpr int kGradV = 128;  // vocabulary entries per workgroup of the LoRA-gradient pass
+inline int grad_parts(int V) { return (V + kGradV - 1) / kGradV; }
 
 struct UpdateArgs {
     const void *W;          // packed lm_head [V][d]
@@ -227,7 +228,7 @@ struct UpdateArgs {
     float *row_stats;       // [n][8]
     float *dA;              // [V][r]
     float *du;              // [n][r]
-    float *du_part;         // [n][kDuSlices][r] scratch: du over slices of the vocabulary
+    float *du_part;         // [grad_parts(V)][n][16] scratch: du shares of the vocabulary blocks
     float *dB;              // [r][d]
     float *loss_out;        // [16]: loss, kl, ce, pg, entropy, n, n_acc, n_fresh, n_fresh_acc | counts at [12..16)
 };

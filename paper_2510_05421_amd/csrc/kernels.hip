@@ -292,11 +292,12 @@ __global__ void __launch_bounds__(256) rms_rows_kernel(const float *ss, int ld_s
 
 // ------------------------------------------------------------------------------------------
 // Large-M GEMM staged through LDS (prefill blocks, the drafter update's replay rows).  Workgroup
-// tile: 128 tokens x 256 features, eight waves as 2 x 4, wave (wy, wx) owning tokens 64 wy .. +63
-// (four 16-token groups) and features 64 wx .. +63 (four tiles): 16 MFMA tiles, two waves per
-// SIMD, so one wave's LDS reads run under the other's MFMAs (8 x 2048-token prefill 0.33 -> 0.28 s
-// against four waves of 32 tiles).  Per K chunk the workgroup needs 8 activation and 16 weight
-// fragments (1 KiB each, fragment-major in memory and kept so in LDS).  They travel from memory
+// tile of prefill blocks: 128 tokens x 256 features, eight waves as 2 x 4, wave (wy, wx) owning
+// tokens 64 wy .. +63 (four 16-token groups) and features 64 wx .. +63 (four tiles): 16 MFMA tiles,
+// two waves per SIMD, so one wave's LDS reads run under the other's MFMAs (8 x 2048-token prefill
+// 0.33 -> 0.28 s against four waves of 32 tiles).  Per K chunk the workgroup needs 8 activation and
+// 16 weight fragments (1 KiB each, fragment-major in memory and kept so in LDS); at up to 256 rows
+// the tile is 256 tokens x 128 features (waves 4 x 2, 16 activation and 8 weight fragments).  They travel from memory
 // straight into an LDS ring of NS stages with direct-to-LDS loads (each wave loads 3 fragments of
 // every stage), so NS - 1 chunks are in flight while one is multiplied; each wave reads its 4 + 4
 // fragments of the chunk from LDS.  Three stages (72 KiB) let two workgroups share a compute unit
@@ -359,12 +360,84 @@ __device__ __forceinline__ void lds_fragments(uint32_t xa, uint32_t wa, uint4 (&
     wf[0] = as_uint4(w0); wf[1] = as_uint4(w1); wf[2] = as_uint4(w2); wf[3] = as_uint4(w3);
 }
 
-// WV waves: 4 as 2 x 2 (wave tile 64 tokens x 128 features), or 8 as 2 x 4 (64 tokens x 64
-// features: two waves per SIMD, so one wave's LDS reads run under the other's MFMAs).
-template <DType T, int EPI, int WV>
+// Logits epilogue of the large-M GEMM (the drafter update's 65-256 replay rows): for every
+// output z = sc * acc + gamma * sum_c A_s[n][c] u[m][c], the LoRA sum taken over the rank in
+// increasing order from zero, as the decode GEMM's epilogue takes it.  The workgroup's rows of u
+// and of A_s go into LDS (the ring is free once the K loop is done), 32 rank columns at a time,
+// so each lane reads its factors from LDS instead of gathering them from memory, and the lane's
+// four consecutive logits of a row group leave in one 16-byte store.  Writes logits only: no
+// argmax partials, no sampling (the update asks for neither).
+template <int WV, int XF, int WF, int NW>
+__device__ __forceinline__ void lds_logits_epilogue(const GemmArgs &a, const f32x4 (&acc)[NW][4], float *smem,
+                                                    int g0, int t0, int wy, int wx) {
+    constexpr int RS = 32, LD = RS + 1;  // rank columns per pass; padded row stride in floats
+    const int lane = threadIdx.x & 63, G4 = lane >> 4;
+    const int NT = a.N / 16;
+    const int m_base = 16 * g0, n_base = 16 * t0;
+    float *us = smem;                // [16 XF rows][LD]
+    float *as = smem + 16 * XF * LD;  // [16 WF rows][LD]
+    float sacc[NW][4][4];
+#pragma unroll
+    for (int t = 0; t < NW; ++t)
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) sacc[t][g][j] = 0.f;
+    const int r = a.lora_A != nullptr ? a.r : 0;
+    for (int c0 = 0; c0 < r; c0 += RS) {
+        const int rc = min(RS, r - c0);
+        __syncthreads();  // every wave is done with the LDS it read before (ring or last pass)
+        for (int i = threadIdx.x; i < 16 * XF * rc; i += 64 * WV) {
+            const int row = i / rc, c = i - row * rc;
+            us[row * LD + c] = a.lora_u[(size_t)min(m_base + row, a.M - 1) * a.r + c0 + c];
+        }
+        for (int i = threadIdx.x; i < 16 * WF * rc; i += 64 * WV) {
+            const int row = i / rc, c = i - row * rc;
+            as[row * LD + c] = a.lora_A[(size_t)min(n_base + row, NT * 16 - 1) * a.r + c0 + c];
+        }
+        __syncthreads();
+        for (int c = 0; c < rc; ++c) {
+            float uv[4];
+#pragma unroll
+            for (int g = 0; g < 4; ++g) uv[g] = us[(16 * (4 * wy + g) + (lane & 15)) * LD + c];
+#pragma unroll
+            for (int t = 0; t < NW; ++t)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const float av = as[(16 * (NW * wx + t) + 4 * G4 + j) * LD + c];
+#pragma unroll
+                    for (int g = 0; g < 4; ++g) sacc[t][g][j] += av * uv[g];
+                }
+        }
+    }
+#pragma unroll
+    for (int t = 0; t < NW; ++t) {
+        const int nt = t0 + NW * wx + t;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            const int m = m_base + 16 * (4 * wy + g) + (lane & 15);
+            if (nt < NT && m < a.M) {
+                const float sc = a.ss_in != nullptr ? a.sinv_rows[m] : 1.0f;
+                float y[4];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    y[j] = acc[t][g][j] * sc;
+                    if (r > 0) y[j] = y[j] + a.gamma * sacc[t][g][j];
+                }
+                *(float4 *)(a.Z + (size_t)m * a.N + nt * 16 + 4 * G4) = make_float4(y[0], y[1], y[2], y[3]);
+            }
+        }
+    }
+}
+
+// WV waves as WY (tokens) x WX (features), every wave tile 64 tokens x 16 NW features.  A stage
+// holds FR = 24 fragments: XF = 4 WY activation groups and WF = FR - XF weight tiles.
+template <DType T, int EPI, int WV, int WY>
 __global__ void __launch_bounds__(64 * WV) gemm_lds_kernel(GemmArgs a, int n_tok_tiles, int n_tiles_total) {
     constexpr int NS = kLdsStages, FR = 24, PER = FR / WV;  // stages, fragments per stage, per wave
-    constexpr int WX = WV / 2, NW = 16 / WX;                // waves across the features; tiles per wave
+    constexpr int XF = 4 * WY, WF = FR - XF;                // activation groups, weight tiles per stage
+    constexpr int WX = WV / WY, NW = WF / WX;               // waves across the features; tiles per wave
+    static_assert(WX * WY == WV && NW * WX == WF && PER * WV == FR, "workgroup shape");
     constexpr uint32_t kStage = FR * 1024;
     __shared__ __align__(1024) uint4 ring[NS][FR][64];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -376,15 +449,15 @@ __global__ void __launch_bounds__(64 * WV) gemm_lds_kernel(GemmArgs a, int n_tok
     const int j = blockIdx.x >> 3;
     const int tl = (blockIdx.x & 7) * per + j;
     if (j >= per || tl >= n_tiles_total) return;  // uniform across the workgroup (before any barrier)
-    const int g0 = (tl % n_tok_tiles) * 8, t0 = (tl / n_tok_tiles) * 16;
-    // the fragments this wave loads into every stage: f = PER * wave + i; f < 8: activation group
-    // g0 + f, else weight tile t0 + f - 8 (clamped into range)
+    const int g0 = (tl % n_tok_tiles) * XF, t0 = (tl / n_tok_tiles) * WF;
+    // the fragments this wave loads into every stage: f = PER * wave + i; f < XF: activation group
+    // g0 + f, else weight tile t0 + f - XF (clamped into range)
     const uint4 *src[PER];
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
         const int f = PER * wave + i;
-        src[i] = (f < 8 ? (const uint4 *)a.X + (size_t)min(g0 + f, NG - 1) * KT * 64
-                        : (const uint4 *)a.W + (size_t)min(t0 + f - 8, NT - 1) * KT * 64) + lane;
+        src[i] = (f < XF ? (const uint4 *)a.X + (size_t)min(g0 + f, NG - 1) * KT * 64
+                         : (const uint4 *)a.W + (size_t)min(t0 + f - XF, NT - 1) * KT * 64) + lane;
     }
     lds_u8 *const ring0 = (lds_u8 *)&ring[0][0][0];
     auto issue = [&](int st, int k) {
@@ -420,11 +493,15 @@ __global__ void __launch_bounds__(64 * WV) gemm_lds_kernel(GemmArgs a, int n_tok
         if (k + NS - 1 < KT) issue((k + NS - 1) % NS, k + NS - 1);
         const uint32_t sb = lbase + (uint32_t)(k % NS) * kStage;
         uint4 xf[4], wf[NW];
-        lds_fragments<NW>(sb + 4 * wy * 1024, sb + (8 + NW * wx) * 1024, xf, wf);
+        lds_fragments<NW>(sb + 4 * wy * 1024, sb + (XF + NW * wx) * 1024, xf, wf);
 #pragma unroll
         for (int t = 0; t < NW; ++t)
 #pragma unroll
             for (int g = 0; g < 4; ++g) acc[t][g] = St<T>::mma(wf[t], xf[g], acc[t][g]);
+    }
+    if constexpr (EPI == EPI_LOGITS) {
+        lds_logits_epilogue<WV, XF, WF, NW>(a, acc, (float *)&ring[0][0][0], g0, t0, wy, wx);
+        return;
     }
     const int gw = g0 + 4 * wy;
     if (gw >= NG) return;  // uniform across the wave
@@ -432,23 +509,33 @@ __global__ void __launch_bounds__(64 * WV) gemm_lds_kernel(GemmArgs a, int n_tok
 #pragma unroll
     for (int t = 0; t < NW; ++t) {
         const int nt = t0 + NW * wx + t;
-        if (nt >= NT) break;  // uniform
-        EpiOperands<4> pre;
-        epilogue_prefetch<4, EPI>(a, nt, pre, m0);
-        epilogue_prefetch_rope<4, EPI>(a, nt, pre);
-        gemm_epilogue<T, 4, EPI>(a, nt, acc[t], a.sinv_rows + m0, pre, m0);
+        if (nt < NT) {  // uniform; a guard, not a break, so the loop unrolls and acc stays in registers
+            EpiOperands<4> pre;
+            epilogue_prefetch<4, EPI>(a, nt, pre, m0);
+            epilogue_prefetch_rope<4, EPI>(a, nt, pre);
+            gemm_epilogue<T, 4, EPI>(a, nt, acc[t], a.sinv_rows + m0, pre, m0);
+        }
     }
+}
+
+template <DType T, int EPI, int WY>
+static void launch_gemm_lds_shape(const GemmArgs &a, hipStream_t s, const LaunchEvents &ev) {
+    constexpr int WV = kLdsWaves, XF = 4 * WY, WF = 24 - XF;
+    const int tok = (a.M + 16 * XF - 1) / (16 * XF), blk = (a.N / 16 + WF - 1) / WF, total = tok * blk;
+    const int grid = 8 * ((total + 7) / 8);
+    if (ev.start || ev.stop)
+        hipExtLaunchKernelGGL(gemm_lds_kernel<T, EPI, WV, WY>, dim3(grid), dim3(64 * WV), 0, s, ev.start, ev.stop, 0, a, tok, total);
+    else
+        gemm_lds_kernel<T, EPI, WV, WY><<<grid, 64 * WV, 0, s>>>(a, tok, total);
 }
 
 template <DType T, int EPI>
 static void launch_gemm_lds(const GemmArgs &a, hipStream_t s, const LaunchEvents &ev) {
-    constexpr int WV = kLdsWaves;
-    const int tok = (a.M + 127) / 128, blk = (a.N / 16 + 15) / 16, total = tok * blk;
-    const int grid = 8 * ((total + 7) / 8);
-    if (ev.start || ev.stop)
-        hipExtLaunchKernelGGL(gemm_lds_kernel<T, EPI, WV>, dim3(grid), dim3(64 * WV), 0, s, ev.start, ev.stop, 0, a, tok, total);
-    else
-        gemm_lds_kernel<T, EPI, WV><<<grid, 64 * WV, 0, s>>>(a, tok, total);
+    // up to 256 rows (the drafter update): one token tile of 256 rows, so each weight block is read
+    // by one workgroup (update forward 94 -> 91 us at the 7B head, full-ring update 0.450 ->
+    // 0.409 ms); prefill blocks: 128 rows x 256 features
+    if (a.M <= 256) launch_gemm_lds_shape<T, EPI, 4>(a, s, ev);
+    else launch_gemm_lds_shape<T, EPI, 2>(a, s, ev);
 }
 
 template <DType T>
@@ -1573,16 +1660,27 @@ __device__ __forceinline__ float block_max1024(float v, float *lds16) {
     return s;
 }
 
+// The row kernel (see above): thread t takes entries v = t + 1024 e in order; the first NE of them
+// (e < NE) are read once into registers and serve all three passes, any beyond 1024 NE are read
+// from memory in each pass, with the same arithmetic (7B ring of 256 rows: 54.8 -> 36.5 us).
+template <int NE>
 __global__ void __launch_bounds__(1024) upd_rows_kernel(UpdateArgs u, const float *counts) {
     __shared__ float red[16];
     const int i = blockIdx.x;
     float *z = u.Z + (size_t)i * u.V;
     const float *lg = u.logits + (size_t)i * u.V;
     const float itau = 1.0f / u.tau;
+    const int tail = threadIdx.x + 1024 * NE;  // first entry read from memory in every pass
+    float zr[NE], qr[NE];
+#pragma unroll
+    for (int e = 0; e < NE; ++e) {
+        const int v = min((int)threadIdx.x + 1024 * e, u.V - 1);  // entries past V are never used
+        zr[e] = z[v];
+        qr[e] = lg[v] * itau;
+    }
     // per-thread running maximum and rescaled sum of both distributions
     float mz = -INFINITY, mq = -INFINITY, sz = 0.f, sq = 0.f;
-    for (int v = threadIdx.x; v < u.V; v += 1024) {
-        const float a = z[v], b = lg[v] * itau;
+    auto online = [&](float a, float b) {
         if (a > mz) {
             sz = sz * expf(mz - a) + 1.f;
             mz = a;
@@ -1595,18 +1693,26 @@ __global__ void __launch_bounds__(1024) upd_rows_kernel(UpdateArgs u, const floa
         } else {
             sq += expf(b - mq);
         }
-    }
+    };
+#pragma unroll
+    for (int e = 0; e < NE; ++e)
+        if ((int)threadIdx.x + 1024 * e < u.V) online(zr[e], qr[e]);
+    for (int v = tail; v < u.V; v += 1024) online(z[v], lg[v] * itau);
     const float Mz = block_max1024(mz, red), Mq = block_max1024(mq, red);
     sz = block_sum1024(mz == -INFINITY ? 0.f : sz * expf(mz - Mz), red);
     sq = block_sum1024(mq == -INFINITY ? 0.f : sq * expf(mq - Mq), red);
     const float lz = Mz + logf(sz), lq = Mq + logf(sq);
     float kl = 0.f, ent = 0.f;
-    for (int v = threadIdx.x; v < u.V; v += 1024) {
-        const float lp = z[v] - lz, lqv = lg[v] * itau - lq;
+    auto klent = [&](float zv, float qv) {
+        const float lp = zv - lz, lqv = qv - lq;
         const float p = expf(lp);
         kl += p * (lp - lqv);
         ent -= p * lp;
-    }
+    };
+#pragma unroll
+    for (int e = 0; e < NE; ++e)
+        if ((int)threadIdx.x + 1024 * e < u.V) klent(zr[e], qr[e]);
+    for (int v = tail; v < u.V; v += 1024) klent(z[v], lg[v] * itau);
     kl = block_sum1024(kl, red);
     ent = block_sum1024(ent, red);
     const int ai = u.a[i];
@@ -1617,12 +1723,17 @@ __global__ void __launch_bounds__(1024) upd_rows_kernel(UpdateArgs u, const floa
     const float beta = u.c_ce * ri / fmaxf(na, 1.f) + u.c_pg * (ri - u.baseline) * fi / fmaxf(nf, 1.f);
     const float eps = u.c_ent / n;
     __syncthreads();  // every thread has read z[ai] before it is overwritten
-    for (int v = threadIdx.x; v < u.V; v += 1024) {
-        const float lp = z[v] - lz, lqv = lg[v] * itau - lq;
+    auto grad = [&](int v, float zv, float qv) {
+        const float lp = zv - lz, lqv = qv - lq;
         const float p = expf(lp);
-        const float g = alpha * p * (lp - lqv - kl) + beta * (p - (v == ai ? 1.f : 0.f)) + eps * p * (lp + ent);
-        z[v] = g;
+        z[v] = alpha * p * (lp - lqv - kl) + beta * (p - (v == ai ? 1.f : 0.f)) + eps * p * (lp + ent);
+    };
+#pragma unroll
+    for (int e = 0; e < NE; ++e) {
+        const int v = (int)threadIdx.x + 1024 * e;
+        if (v < u.V) grad(v, zr[e], qr[e]);
     }
+    for (int v = tail; v < u.V; v += 1024) grad(v, z[v], lg[v] * itau);
     if (threadIdx.x == 0) {
         float *st = u.row_stats + (size_t)i * 8;
         st[0] = kl;
@@ -1662,116 +1773,187 @@ __global__ void upd_loss_kernel(UpdateArgs u, const float *counts) {
     u.loss_out[8] = counts[3];
 }
 
-// The LoRA gradients run with a fixed 64-slot accumulator per thread (rank <= 64), fully
-// unrolled and guarded by the rank so the slots stay in registers.
-constexpr int kMaxRank = 64;
-
-// dA[v][c] = gamma * sum_i g[i][v] u[i][c].  A workgroup takes 64 vocabulary rows (lane = row);
-// wave w takes the ranks c = w, w+4, ...  Rows i are taken 16 at a time with all 16 loads of g
-// in flight; each output is one sum over i in order.
-__global__ void __launch_bounds__(256) upd_dA_kernel(UpdateArgs u) {
-    constexpr int CPW = kMaxRank / 4;
-    const int lane = threadIdx.x & 63;
-    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int v = blockIdx.x * 64 + lane;
-    const int vv = min(v, u.V - 1);
-    float acc[CPW];
+// Sums p[0..15] over the 64 lanes of the wave, all sixteen at once: four halving steps each hand
+// half of the carried values to the lane 32, 16, 8 apart and then to the mirror lane of the
+// 8-lane half row (lane ^ 7), keeping the other half; two plain steps add within the quad.  Lane l
+// returns the total of value l >> 2.  The tree is fixed, so the sums are deterministic.
+__device__ __forceinline__ float transpose_sum16(const float (&p)[16], int lane) {
+    const bool h32 = lane & 32, h16 = lane & 16, h8 = lane & 8, h4 = lane & 4;
+    float q[8], r[4], t[2];
 #pragma unroll
-    for (int k = 0; k < CPW; ++k) acc[k] = 0.f;
-    for (int i0 = 0; i0 < u.n; i0 += 16) {
-        float g[16];
+    for (int k = 0; k < 8; ++k) q[k] = (h32 ? p[k + 8] : p[k]) + __shfl_xor(h32 ? p[k] : p[k + 8], 32);
 #pragma unroll
-        for (int j = 0; j < 16; ++j) g[j] = u.Z[(size_t)min(i0 + j, u.n - 1) * u.V + vv];
+    for (int k = 0; k < 4; ++k) r[k] = (h16 ? q[k + 4] : q[k]) + __shfl_xor(h16 ? q[k] : q[k + 4], 16);
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
-            if (i0 + j >= u.n) break;  // uniform
-            const float *ui = u.u + (size_t)(i0 + j) * u.rank;
-#pragma unroll
-            for (int k = 0; k < CPW; ++k)
-                if (w + 4 * k < u.rank) acc[k] += g[j] * ui[w + 4 * k];
-        }
-    }
-    if (v < u.V)
-#pragma unroll
-        for (int k = 0; k < CPW; ++k)
-            if (w + 4 * k < u.rank) u.dA[(size_t)v * u.rank + w + 4 * k] = u.gamma * acc[k];
+    for (int k = 0; k < 2; ++k) t[k] = (h8 ? r[k + 2] : r[k]) + dpp_f32<0x128>(h8 ? r[k] : r[k + 2]);  // row_ror 8
+    float v = (h4 ? t[1] : t[0]) + dpp_f32<0x141>(h4 ? t[0] : t[1]);  // half-row mirror
+    v += dpp_f32<0xB1>(v);
+    v += dpp_f32<0x4E>(v);
+    return v;
 }
 
-// du[i][c] = gamma * sum_v A[v][c] g[i][v], in two passes.  Pass 1: workgroup (i, s) sums the
-// vocabulary slice s (kDuSlices slices); thread t takes v = t, t+256, ... of the slice, four at a
-// time with their loads in flight, and the 256 partial vectors are summed in a fixed tree
-// (butterfly per wave, then the waves in order).  Pass 2 adds the slices in order.
-__global__ void __launch_bounds__(256) upd_du_kernel(UpdateArgs u) {
-    __shared__ float part[4][kMaxRank + 1];
-    const int i = blockIdx.x, s = blockIdx.y, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const int span = (u.V + kDuSlices - 1) / kDuSlices;
-    const int v0 = s * span, v1 = min(u.V, v0 + span);
-    float acc[kMaxRank];
+// Rows rb .. rb + 255 of the ranks c0 .. c0 + 15 of a row-major [n][rank] matrix into LDS, 16
+// floats per row, zero past the rank and past n (so the readers need no guards).
+__device__ __forceinline__ void stage_rank_slice(float (&dst)[256][16], const float *src, int n, int rank, int rb,
+                                                 int c0, int nthreads) {
+    for (int e = threadIdx.x; e < 256 * 16; e += nthreads) {
+        const int row = e >> 4, c = e & 15, i = rb + row;
+        dst[row][c] = (i < n && c0 + c < rank) ? src[(size_t)i * rank + c0 + c] : 0.f;
+    }
+}
+
+// dA[v][c] = gamma sum_i g[i][v] u[i][c] and du[i][c] = gamma sum_v A_s[v][c] g[i][v], g = dL/dz
+// (the rows of Z after upd_rows_kernel), in one pass over g for the 16 ranks c0 .. c0 + 15.  A
+// workgroup takes kGradV = 128 vocabulary entries, two per lane (v0 = 128 b + 2 l, v0 + 1), and
+// every row: per block of 256 rows, the block's u slice goes to LDS and wave w takes rows 32 w ..
+// 32 w + 31 of the block, eight rows' loads of g in flight.  A lane keeps its two entries' rows
+// of A_s and their 16 dA sums (its rows in order; the eight waves are then added in order through
+// LDS).  Per row it forms the two entries' share of du for the 16 ranks, which transpose_sum16
+// reduces over the wave, and the workgroup's share goes to du_part[b][i][16]; upd_du_sum_kernel
+// adds the workgroups' shares.  g and A_s are each read once (V even, as every vocabulary here
+// is a multiple of 16).
+constexpr int kGradWaves = 8;
+
+__global__ void __launch_bounds__(64 * kGradWaves) upd_grad_kernel(UpdateArgs u, int c0) {
+    __shared__ float red[kGradWaves][kGradV][17];
+    __shared__ __align__(16) float us[256][16];
+    const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int b = blockIdx.x, v0 = b * kGradV + 2 * lane;
+    const int rc = min(16, u.rank - c0);
+    const bool in0 = v0 < u.V, in1 = v0 + 1 < u.V;
+    const size_t vc = (size_t)min(v0, u.V - 2);  // lanes past V read an in-range pair, weighted 0
+    float a0[16], a1[16], d0[16], d1[16];
 #pragma unroll
-    for (int c = 0; c < kMaxRank; ++c) acc[c] = 0.f;
-    const float *g = u.Z + (size_t)i * u.V;
-    const bool vec = (u.rank & 3) == 0;
-    for (int vb = v0 + threadIdx.x; vb < v1; vb += 4 * 256) {
-        // rows past the slice read its last row and enter with weight 0
-        float gv[4];
+    for (int c = 0; c < 16; ++c) {
+        const int cc = c0 + min(c, rc - 1);  // in range even where the value is not used
+        a0[c] = (in0 && c < rc) ? u.A[(size_t)min(v0, u.V - 1) * u.rank + cc] : 0.f;
+        a1[c] = (in1 && c < rc) ? u.A[(size_t)min(v0 + 1, u.V - 1) * u.rank + cc] : 0.f;
+        d0[c] = 0.f;
+        d1[c] = 0.f;
+    }
+    for (int rb = 0; rb < u.n; rb += 256) {
+        __syncthreads();  // every wave is done with the previous block's slice
+        stage_rank_slice(us, u.u, u.n, u.rank, rb, c0, 64 * kGradWaves);
+        __syncthreads();
+        const int i0 = min(u.n, rb + 32 * w), i1 = min(u.n, i0 + 32);
+        for (int ib = i0; ib < i1; ib += 8) {
+            float2 g2[8];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int v = vb + 256 * q;
-            const float gl = g[min(v, v1 - 1)];
-            gv[q] = v < v1 ? gl : 0.f;
-        }
+            for (int k = 0; k < 8; ++k) g2[k] = *(const float2 *)(u.Z + (size_t)min(ib + k, i1 - 1) * u.V + vc);
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const float *Av = u.A + (size_t)min(vb + 256 * q, v1 - 1) * u.rank;
-            if (vec) {
+            for (int k = 0; k < 8; ++k) {
+                const int i = ib + k;
+                if (i < i1) {  // uniform; a guard, not a break, so the loop unrolls
+                    const float g0 = in0 ? g2[k].x : 0.f, g1 = in1 ? g2[k].y : 0.f;
+                    const float4 *ur = (const float4 *)us[i - rb];
+                    float uc[16];
 #pragma unroll
-                for (int c4 = 0; c4 < kMaxRank / 4; ++c4)
-                    if (4 * c4 < u.rank) {
-                        const float4 a4 = ((const float4 *)Av)[c4];
-                        acc[4 * c4 + 0] += a4.x * gv[q];
-                        acc[4 * c4 + 1] += a4.y * gv[q];
-                        acc[4 * c4 + 2] += a4.z * gv[q];
-                        acc[4 * c4 + 3] += a4.w * gv[q];
+                    for (int q = 0; q < 4; ++q) {
+                        const float4 t = ur[q];
+                        uc[4 * q] = t.x;
+                        uc[4 * q + 1] = t.y;
+                        uc[4 * q + 2] = t.z;
+                        uc[4 * q + 3] = t.w;
                     }
-            } else {
+                    float p[16];
 #pragma unroll
-                for (int c = 0; c < kMaxRank; ++c)
-                    if (c < u.rank) acc[c] += Av[c] * gv[q];
+                    for (int c = 0; c < 16; ++c) {
+                        d0[c] += g0 * uc[c];
+                        d1[c] += g1 * uc[c];
+                        p[c] = a0[c] * g0 + a1[c] * g1;
+                    }
+                    const float sdu = transpose_sum16(p, lane);
+                    if ((lane & 3) == 0) u.du_part[((size_t)b * u.n + i) * 16 + (lane >> 2)] = sdu;
+                }
             }
         }
     }
 #pragma unroll
-    for (int c = 0; c < kMaxRank; ++c)
-        if (c < u.rank) {
-            const float sw = wave_sum(acc[c]);
-            if (lane == 0) part[w][c] = sw;
-        }
+    for (int c = 0; c < 16; ++c) {
+        red[w][2 * lane][c] = d0[c];
+        red[w][2 * lane + 1][c] = d1[c];
+    }
     __syncthreads();
-    if (threadIdx.x < u.rank) {
+    for (int e = threadIdx.x; e < kGradV * 16; e += 64 * kGradWaves) {
+        const int vv = e >> 4, c = e & 15, v = b * kGradV + vv;
+        if (c >= rc || v >= u.V) continue;
         float t = 0.f;
-        for (int k = 0; k < 4; ++k) t += part[k][threadIdx.x];
-        u.du_part[((size_t)i * kDuSlices + s) * u.rank + threadIdx.x] = t;
+#pragma unroll
+        for (int k = 0; k < kGradWaves; ++k) t += red[k][vv][c];
+        u.dA[(size_t)v * u.rank + c0 + c] = u.gamma * t;
     }
 }
 
-__global__ void upd_du_sum_kernel(UpdateArgs u) {
-    const int e = blockIdx.x * blockDim.x + threadIdx.x;
-    if (e >= u.n * u.rank) return;
-    const int i = e / u.rank, c = e - i * u.rank;
+// du[i][c0 + c] = gamma * (sum of the nb workgroups' shares du_part[b][i][c]).  One workgroup
+// per row; thread (j, c) adds the shares of workgroups [j P, (j + 1) P) in order (P = ceil(nb /
+// 16)), then the sixteen partial sums are added in order.
+__global__ void __launch_bounds__(256) upd_du_sum_kernel(UpdateArgs u, int c0, int nb) {
+    __shared__ float part[16][17];
+    const int i = blockIdx.x, c = threadIdx.x & 15, j = threadIdx.x >> 4;
+    const int per = (nb + 15) / 16, b0 = min(nb, j * per), b1 = min(nb, b0 + per);
     float t = 0.f;
-    for (int s = 0; s < kDuSlices; ++s) t += u.du_part[((size_t)i * kDuSlices + s) * u.rank + c];
-    u.du[e] = u.gamma * t;
+    for (int bb = b0; bb < b1; ++bb) t += u.du_part[((size_t)bb * u.n + i) * 16 + c];
+    part[j][c] = t;
+    __syncthreads();
+    if (j == 0 && c < min(16, u.rank - c0)) {
+        float sum = 0.f;
+#pragma unroll
+        for (int k = 0; k < 16; ++k) sum += part[k][c];
+        u.du[(size_t)i * u.rank + c0 + c] = u.gamma * sum;
+    }
 }
 
-// dB[c][k] = sum_i du[i][c] h[i][k]   (one thread per (k, c); rows i in order)
+// dB[c][k] = sum_i du[i][c] h[i][k] for the 16 ranks c0 .. c0 + 15: lane = k (64 per wave); per
+// block of 256 rows the block's du slice goes to LDS and wave w of eight takes rows 32 w .. 32 w +
+// 31 of the block, eight rows' loads of h in flight.  The eight waves' sums are added in order
+// through LDS.  h is read once per pass.
 template <DType T>
-__global__ void __launch_bounds__(256) upd_dB_kernel(UpdateArgs u) {
-    const int k = blockIdx.x * 256 + threadIdx.x, c = blockIdx.y;
-    if (k >= u.d) return;
-    float acc = 0.f;
-#pragma unroll 4
-    for (int i = 0; i < u.n; ++i) acc += u.du[(size_t)i * u.rank + c] * St<T>::load(u.Hh, (size_t)i * u.d + k);
-    u.dB[(size_t)c * u.d + k] = acc;
+__global__ void __launch_bounds__(512) upd_dB_kernel(UpdateArgs u, int c0) {
+    __shared__ float red[8][64][17];
+    __shared__ __align__(16) float ds[256][16];
+    const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int k = blockIdx.x * 64 + lane, kk = min(k, u.d - 1);
+    const int rc = min(16, u.rank - c0);
+    float acc[16];
+#pragma unroll
+    for (int c = 0; c < 16; ++c) acc[c] = 0.f;
+    for (int rb = 0; rb < u.n; rb += 256) {
+        __syncthreads();  // every wave is done with the previous block's slice
+        stage_rank_slice(ds, u.du, u.n, u.rank, rb, c0, 512);
+        __syncthreads();
+        const int i0 = min(u.n, rb + 32 * w), i1 = min(u.n, i0 + 32);
+        for (int ib = i0; ib < i1; ib += 8) {
+            float hv[8];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) hv[q] = St<T>::load(u.Hh, (size_t)min(ib + q, i1 - 1) * u.d + kk);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                const int i = ib + q;
+                if (i < i1) {  // uniform
+                    const float4 *dr = (const float4 *)ds[i - rb];
+#pragma unroll
+                    for (int c4 = 0; c4 < 4; ++c4) {
+                        const float4 t = dr[c4];
+                        acc[4 * c4] += t.x * hv[q];
+                        acc[4 * c4 + 1] += t.y * hv[q];
+                        acc[4 * c4 + 2] += t.z * hv[q];
+                        acc[4 * c4 + 3] += t.w * hv[q];
+                    }
+                }
+            }
+        }
+    }
+#pragma unroll
+    for (int c = 0; c < 16; ++c) red[w][lane][c] = acc[c];
+    __syncthreads();
+    for (int e = threadIdx.x; e < 64 * 16; e += 512) {
+        const int c = e >> 6, kl = e & 63, ko = blockIdx.x * 64 + kl;
+        if (c >= rc || ko >= u.d) continue;
+        float t = 0.f;
+#pragma unroll
+        for (int q = 0; q < 8; ++q) t += red[q][kl][c];
+        u.dB[(size_t)(c0 + c) * u.d + ko] = t;
+    }
 }
 
 void launch_update_forward(DType t, const UpdateArgs &u, hipStream_t s) {
@@ -1820,18 +2002,25 @@ void launch_update_forward(DType t, const UpdateArgs &u, hipStream_t s) {
                 launch_gemm_lds<DType::F32, EPI_LOGITS>(g, s, LaunchEvents{});
         }
     }
-    upd_rows_kernel<<<u.n, 1024, 0, s>>>(u, counts);
+    if (u.V <= 4096)
+        upd_rows_kernel<4><<<u.n, 1024, 0, s>>>(u, counts);
+    else
+        upd_rows_kernel<32><<<u.n, 1024, 0, s>>>(u, counts);
     upd_loss_kernel<<<1, 64, 0, s>>>(u, counts);
 }
 
 void launch_update_backward(DType t, const UpdateArgs &u, hipStream_t s) {
-    upd_dA_kernel<<<(u.V + 63) / 64, 256, 0, s>>>(u);
-    upd_du_kernel<<<dim3(u.n, kDuSlices), 256, 0, s>>>(u);
-    upd_du_sum_kernel<<<(u.n * u.rank + 255) / 256, 256, 0, s>>>(u);
-    if (t == DType::BF16)
-        upd_dB_kernel<DType::BF16><<<dim3((u.d + 255) / 256, u.rank), 256, 0, s>>>(u);
-    else
-        upd_dB_kernel<DType::F32><<<dim3((u.d + 255) / 256, u.rank), 256, 0, s>>>(u);
+    const int nb = grad_parts(u.V);
+    for (int c0 = 0; c0 < u.rank; c0 += 16) {  // 16 ranks per pass over g
+        upd_grad_kernel<<<nb, 64 * kGradWaves, 0, s>>>(u, c0);
+        upd_du_sum_kernel<<<u.n, 256, 0, s>>>(u, c0, nb);
+    }
+    for (int c0 = 0; c0 < u.rank; c0 += 16) {
+        if (t == DType::BF16)
+            upd_dB_kernel<DType::BF16><<<(u.d + 63) / 64, 512, 0, s>>>(u, c0);
+        else
+            upd_dB_kernel<DType::F32><<<(u.d + 63) / 64, 512, 0, s>>>(u, c0);
+    }
 }
 
 __global__ void adam_kernel(float *p, const float *g, float *m, float *v, int n, float lr, float b1, float b2, float eps,
