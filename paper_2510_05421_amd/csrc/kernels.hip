@@ -322,39 +322,43 @@ __device__ __forceinline__ void wait_vmcnt() {
 
 typedef __attribute__((address_space(3))) uint8_t lds_u8;
 
-// 16 bytes of LDS at byte address addr + OFF, and the wait for all of a wave's LDS reads; the
-// wait names the loaded registers so nothing that uses them can move above it.
 typedef unsigned v4u32 __attribute__((ext_vector_type(4)));
-
-template <int OFF>
-__device__ __forceinline__ v4u32 lds_read16(uint32_t addr) {
-    v4u32 v;
-    asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "i"(OFF));
-    return v;
-}
-
 __device__ __forceinline__ uint4 as_uint4(v4u32 v) { return uint4{v.x, v.y, v.z, v.w}; }
 
 // The wave's fragments of one chunk, read from LDS and awaited: 4 activation groups at xa and NW
-// weight tiles at wa (byte addresses; fragment i is i KiB further).  The wait names the loaded
-// registers so nothing that uses them moves above it.
+// weight tiles at wa (byte addresses; fragment i is i KiB further).  The reads and the wait are
+// one asm statement, so nothing can use (or copy) a register before its read has completed; the
+// outputs are early-clobber so none of them overwrites an address a later read still needs.
 template <int NW>
 __device__ __forceinline__ void lds_fragments(uint32_t xa, uint32_t wa, uint4 (&xf)[4], uint4 (&wf)[NW]) {
-    v4u32 x0 = lds_read16<0>(xa), x1 = lds_read16<1024>(xa), x2 = lds_read16<2048>(xa), x3 = lds_read16<3072>(xa);
-    v4u32 w0 = lds_read16<0>(wa), w1 = lds_read16<1024>(wa), w2 = lds_read16<2048>(wa), w3 = lds_read16<3072>(wa);
+    v4u32 x0, x1, x2, x3, w0, w1, w2, w3;
     if constexpr (NW == 8) {
-        v4u32 w4 = lds_read16<4096>(wa), w5 = lds_read16<5120>(wa), w6 = lds_read16<6144>(wa), w7 = lds_read16<7168>(wa);
-        asm volatile("s_waitcnt lgkmcnt(0)"
-                     : "+v"(x0), "+v"(x1), "+v"(x2), "+v"(x3), "+v"(w0), "+v"(w1), "+v"(w2), "+v"(w3), "+v"(w4),
-                       "+v"(w5), "+v"(w6), "+v"(w7));
+        v4u32 w4, w5, w6, w7;
+        asm volatile(
+            "ds_read_b128 %0, %12 offset:0\n\tds_read_b128 %1, %12 offset:1024\n\t"
+            "ds_read_b128 %2, %12 offset:2048\n\tds_read_b128 %3, %12 offset:3072\n\t"
+            "ds_read_b128 %4, %13 offset:0\n\tds_read_b128 %5, %13 offset:1024\n\t"
+            "ds_read_b128 %6, %13 offset:2048\n\tds_read_b128 %7, %13 offset:3072\n\t"
+            "ds_read_b128 %8, %13 offset:4096\n\tds_read_b128 %9, %13 offset:5120\n\t"
+            "ds_read_b128 %10, %13 offset:6144\n\tds_read_b128 %11, %13 offset:7168\n\t"
+            "s_waitcnt lgkmcnt(0)"
+            : "=&v"(x0), "=&v"(x1), "=&v"(x2), "=&v"(x3), "=&v"(w0), "=&v"(w1), "=&v"(w2), "=&v"(w3),
+              "=&v"(w4), "=&v"(w5), "=&v"(w6), "=&v"(w7)
+            : "v"(xa), "v"(wa));
         wf[4] = as_uint4(w4);
         wf[5] = as_uint4(w5);
         wf[6] = as_uint4(w6);
         wf[7] = as_uint4(w7);
     } else {
         static_assert(NW == 4, "4 or 8 weight tiles per wave");
-        asm volatile("s_waitcnt lgkmcnt(0)"
-                     : "+v"(x0), "+v"(x1), "+v"(x2), "+v"(x3), "+v"(w0), "+v"(w1), "+v"(w2), "+v"(w3));
+        asm volatile(
+            "ds_read_b128 %0, %8 offset:0\n\tds_read_b128 %1, %8 offset:1024\n\t"
+            "ds_read_b128 %2, %8 offset:2048\n\tds_read_b128 %3, %8 offset:3072\n\t"
+            "ds_read_b128 %4, %9 offset:0\n\tds_read_b128 %5, %9 offset:1024\n\t"
+            "ds_read_b128 %6, %9 offset:2048\n\tds_read_b128 %7, %9 offset:3072\n\t"
+            "s_waitcnt lgkmcnt(0)"
+            : "=&v"(x0), "=&v"(x1), "=&v"(x2), "=&v"(x3), "=&v"(w0), "=&v"(w1), "=&v"(w2), "=&v"(w3)
+            : "v"(xa), "v"(wa));
     }
     xf[0] = as_uint4(x0); xf[1] = as_uint4(x1); xf[2] = as_uint4(x2); xf[3] = as_uint4(x3);
     wf[0] = as_uint4(w0); wf[1] = as_uint4(w1); wf[2] = as_uint4(w2); wf[3] = as_uint4(w3);
