@@ -213,14 +213,19 @@ def test_buffer_rows_hold_the_verify_logits_and_normed_states():
     eng.close()
 
 
-@pytest.mark.parametrize("name,n_rows,r", [("tiny", 48, 16), ("tiny", 100, 16), ("tiny", 300, 16), ("1b_L4", 200, 16),
-                                          ("1b_L4", 256, 16), ("tiny", 100, 20), ("1b_L4", 200, 40),
-                                          ("tiny", 300, 64)])
-def test_drafter_update_gradients_match_oracle(name, n_rows, r):
+@pytest.mark.parametrize("name,n_rows,r,vocab", [("tiny", 48, 16, None), ("tiny", 100, 16, None), ("tiny", 300, 16, None),
+                                                ("1b_L4", 200, 16, None), ("1b_L4", 256, 16, None),
+                                                ("tiny", 100, 20, None), ("1b_L4", 200, 40, None),
+                                                ("tiny", 300, 64, None), ("tiny", 100, 16, 4112)])
+def test_drafter_update_gradients_match_oracle(name, n_rows, r, vocab):
     """Row counts cover the update GEMM's 4-, 8- and 16-group variants and more rows than one
     launch takes (300 > 256).  Ranks other than 16 take the large-M logits epilogue through one
-    partial pass over the rank (20), two passes (40: 32 + 8) and two full passes (64)."""
+    partial pass over the rank (20), two passes (40: 32 + 8) and two full passes (64).  A
+    vocabulary of 4112 = 32 * 128 + 16 leaves the gradient pass's last 128-entry block mostly
+    empty."""
     shape = gu.SHAPES[name].replace(lora_rank=r)
+    if vocab is not None:
+        shape = shape.replace(vocab=vocab)
     eng, w = gu.engine(shape, max_seq=64, lora_A_std=0.02, buffer_rows=max(256, n_rows))
     buf = synth.make_buffer(shape.d_model, shape.vocab, n_rows, seed=11)
     eng.prefill(synth.make_prompts(shape.vocab, 1, 8, 1))
@@ -233,8 +238,8 @@ def test_drafter_update_gradients_match_oracle(name, n_rows, r):
     dA = st["grad_A"].cpu().numpy()
     dB = st["grad_B"].cpu().numpy()
     eA, eB = gu.rel_l2(dA, ref.dA), gu.rel_l2(dB, ref.dB)
-    _say("update %s rows=%d rank=%d: |dA| rel err %.3g, |dB| rel err %.3g, loss %.6g vs %.6g"
-         % (name, n_rows, r, eA, eB, st["loss"], ref.loss))
+    _say("update %s rows=%d rank=%d vocab=%d: |dA| rel err %.3g, |dB| rel err %.3g, loss %.6g vs %.6g"
+         % (name, n_rows, r, shape.vocab, eA, eB, st["loss"], ref.loss))
     assert eA <= 1e-2 and eB <= 1e-2
     assert st["rows"] == n_rows and st["accepted"] == int(buf.r.sum()) and st["fresh"] == int(buf.fresh.sum())
     for key in ("kl", "ce", "pg", "entropy"):
