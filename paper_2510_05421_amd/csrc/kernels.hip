@@ -60,7 +60,7 @@ void launch_pack(DType t, PackSrc srcs, const int32_t *prow, int N, int K, void 
 // producing epilogue wrote.  RMSNorm(h) W^T = (h*g) W^T / rms(h), so no separate pass over h.
 // ------------------------------------------------------------------------------------------
 template <DType T, int MG, int EPI, int RT, int WMAX>
-__global__ void __launch_bounds__(64 * WMAX) gemm_kernel(GemmArgs a) {
+__global__ void __launch_bounds__(64 * WMAX, (MG >= 3 && WMAX == 8 && EPI == EPI_SWIGLU && RT <= 3) ? 4 : 1) gemm_kernel(GemmArgs a) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
     const int nt0 = blockIdx.x * RT;
     // the last workgroup may hold fewer than RT tiles: tiles past N / 16 load nothing and store
@@ -114,8 +114,12 @@ __global__ void __launch_bounds__(64 * WMAX) gemm_kernel(GemmArgs a) {
     // stage st holding chunk c + st: once a stage's MFMAs have issued it is refilled with the
     // chunk S ahead, so S - 1 chunks are always in flight while one is multiplied (the same
     // registers as double-buffering S/2 chunks, with more of them in flight).  Chunks are
-    // accumulated in the wave's rotated order whatever S is.
-    constexpr int S = 4;
+    // accumulated in the wave's rotated order whatever S is.  At 33-64 rows, gate/up workgroups
+    // of up to three tiles take two stages under a register bound (128, the launch bound above)
+    // that fits two workgroups per compute unit instead of one (7B, 64 rows: 62.9 -> 52.7 us);
+    // the other epilogues, and four tiles, spill under that bound (the head at 64 rows: 86 ->
+    // 145 us) and keep four stages.
+    constexpr int S = (MG >= 3 && WMAX == 8 && EPI == EPI_SWIGLU && RT <= 3) ? 2 : 4;
     uint4 w[S][RT], x[S][MG];
     auto fetch = [&](int cb, uint4 (&wf)[RT], uint4 (&xf)[MG]) {
         const bool in = cb < c1;
