@@ -438,16 +438,18 @@ __device__ __forceinline__ void lds_logits_epilogue(const GemmArgs &a, const f32
     }
 }
 
-// WV waves as WY (tokens) x WX (features), every wave tile 64 tokens x 16 NW features.  A stage
-// holds FR = 24 fragments: XF = 4 WY activation groups and WF = FR - XF weight tiles.
-template <DType T, int EPI, int WV, int WY>
+// WV waves as WY (tokens) x WX (features), every wave tile 64 tokens x 16 NW features.  A chunk
+// has FR = 24 fragments: XF = 4 WY activation groups and WF = FR - XF weight tiles.  A ring stage
+// holds CPS consecutive chunks (KT a multiple of CPS), so the workgroup meets at one barrier per
+// CPS chunks.
+template <DType T, int EPI, int WV, int WY, int CPS>
 __global__ void __launch_bounds__(64 * WV) gemm_lds_kernel(GemmArgs a, int n_tok_tiles, int n_tiles_total) {
-    constexpr int NS = kLdsStages, FR = 24, PER = FR / WV;  // stages, fragments per stage, per wave
-    constexpr int XF = 4 * WY, WF = FR - XF;                // activation groups, weight tiles per stage
+    constexpr int NS = kLdsStages, FR = 24, PER = FR / WV;  // stages, fragments per chunk, per wave
+    constexpr int XF = 4 * WY, WF = FR - XF;                // activation groups, weight tiles per chunk
     constexpr int WX = WV / WY, NW = WF / WX;               // waves across the features; tiles per wave
     static_assert(WX * WY == WV && NW * WX == WF && PER * WV == FR, "workgroup shape");
-    constexpr uint32_t kStage = FR * 1024;
-    __shared__ __align__(1024) uint4 ring[NS][FR][64];
+    constexpr uint32_t kChunk = FR * 1024, kStage = CPS * kChunk;
+    __shared__ __align__(1024) uint4 ring[NS][CPS * FR][64];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int wy = wave / WX, wx = wave - wy * WX;
     const int KC = (T == DType::BF16) ? 32 : 16;
@@ -468,12 +470,16 @@ __global__ void __launch_bounds__(64 * WV) gemm_lds_kernel(GemmArgs a, int n_tok
                          : (const uint4 *)a.W + (size_t)min(t0 + f - XF, NT - 1) * KT * 64) + lane;
     }
     lds_u8 *const ring0 = (lds_u8 *)&ring[0][0][0];
+    // stage st <- chunks CPS k .. CPS k + CPS - 1
     auto issue = [&](int st, int k) {
 #pragma unroll
-        for (int i = 0; i < PER; ++i)
-            __builtin_amdgcn_global_load_lds((const void *)(src[i] + (size_t)k * 64),
-                                             (__attribute__((address_space(3))) void *)(ring0 + st * kStage + (PER * wave + i) * 1024),
-                                             16, 0, 0);
+        for (int cc = 0; cc < CPS; ++cc)
+#pragma unroll
+            for (int i = 0; i < PER; ++i)
+                __builtin_amdgcn_global_load_lds((const void *)(src[i] + (size_t)(CPS * k + cc) * 64),
+                                                 (__attribute__((address_space(3))) void *)(ring0 + st * kStage + cc * kChunk +
+                                                                                             (PER * wave + i) * 1024),
+                                                 16, 0, 0);
     };
     // this lane's LDS byte address in fragment 0 of stage 0; fragment f of stage st is f KiB and
     // st stages further
@@ -483,29 +489,33 @@ __global__ void __launch_bounds__(64 * WV) gemm_lds_kernel(GemmArgs a, int n_tok
     for (int t = 0; t < NW; ++t)
 #pragma unroll
         for (int g = 0; g < 4; ++g) acc[t][g] = (f32x4){0.f, 0.f, 0.f, 0.f};
+    const int KS = KT / CPS;  // stages of the K loop
 #pragma unroll
     for (int st = 0; st < NS - 1; ++st)
-        if (st < KT) issue(st, st);
-    for (int k = 0; k < KT; ++k) {
-        // chunk k's loads are done once at most min(NS - 2, KT - 1 - k) later stages are in flight
-        const int later = min(NS - 2, KT - 1 - k);
+        if (st < KS) issue(st, st);
+    for (int k = 0; k < KS; ++k) {
+        // stage k's loads are done once at most min(NS - 2, KS - 1 - k) later stages are in flight
+        const int later = min(NS - 2, KS - 1 - k);
         static_assert(NS - 2 <= 4, "wait cases");
-        if (later >= 4) wait_vmcnt<4 * PER>();
-        else if (later == 3) wait_vmcnt<3 * PER>();
-        else if (later == 2) wait_vmcnt<2 * PER>();
-        else if (later == 1) wait_vmcnt<PER>();
+        if (later >= 4) wait_vmcnt<4 * PER * CPS>();
+        else if (later == 3) wait_vmcnt<3 * PER * CPS>();
+        else if (later == 2) wait_vmcnt<2 * PER * CPS>();
+        else if (later == 1) wait_vmcnt<PER * CPS>();
         else wait_vmcnt<0>();
-        // every wave's fragments of chunk k are in LDS, and every wave is done with the stage the
-        // next issue overwrites (its LDS reads of chunk k - 1 completed before its MFMAs)
+        // every wave's fragments of stage k are in LDS, and every wave is done with the stage the
+        // next issue overwrites (its LDS reads of stage k - 1 completed before its MFMAs)
         __builtin_amdgcn_s_barrier();
-        if (k + NS - 1 < KT) issue((k + NS - 1) % NS, k + NS - 1);
-        const uint32_t sb = lbase + (uint32_t)(k % NS) * kStage;
-        uint4 xf[4], wf[NW];
-        lds_fragments<NW>(sb + 4 * wy * 1024, sb + (XF + NW * wx) * 1024, xf, wf);
+        if (k + NS - 1 < KS) issue((k + NS - 1) % NS, k + NS - 1);
 #pragma unroll
-        for (int t = 0; t < NW; ++t)
+        for (int cc = 0; cc < CPS; ++cc) {
+            const uint32_t sb = lbase + (uint32_t)(k % NS) * kStage + cc * kChunk;
+            uint4 xf[4], wf[NW];
+            lds_fragments<NW>(sb + 4 * wy * 1024, sb + (XF + NW * wx) * 1024, xf, wf);
 #pragma unroll
-            for (int g = 0; g < 4; ++g) acc[t][g] = St<T>::mma(wf[t], xf[g], acc[t][g]);
+            for (int t = 0; t < NW; ++t)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) acc[t][g] = St<T>::mma(wf[t], xf[g], acc[t][g]);
+        }
     }
     if constexpr (EPI == EPI_LOGITS) {
         lds_logits_epilogue<WV, XF, WF, NW>(a, acc, (float *)&ring[0][0][0], g0, t0, wy, wx);
@@ -526,24 +536,28 @@ __global__ void __launch_bounds__(64 * WV) gemm_lds_kernel(GemmArgs a, int n_tok
     }
 }
 
-template <DType T, int EPI, int WY>
+template <DType T, int EPI, int WY, int CPS>
 static void launch_gemm_lds_shape(const GemmArgs &a, hipStream_t s, const LaunchEvents &ev) {
     constexpr int WV = kLdsWaves, XF = 4 * WY, WF = 24 - XF;
     const int tok = (a.M + 16 * XF - 1) / (16 * XF), blk = (a.N / 16 + WF - 1) / WF, total = tok * blk;
     const int grid = 8 * ((total + 7) / 8);
     if (ev.start || ev.stop)
-        hipExtLaunchKernelGGL(gemm_lds_kernel<T, EPI, WV, WY>, dim3(grid), dim3(64 * WV), 0, s, ev.start, ev.stop, 0, a, tok, total);
+        hipExtLaunchKernelGGL(gemm_lds_kernel<T, EPI, WV, WY, CPS>, dim3(grid), dim3(64 * WV), 0, s, ev.start, ev.stop, 0, a, tok, total);
     else
-        gemm_lds_kernel<T, EPI, WV, WY><<<grid, 64 * WV, 0, s>>>(a, tok, total);
+        gemm_lds_kernel<T, EPI, WV, WY, CPS><<<grid, 64 * WV, 0, s>>>(a, tok, total);
 }
 
 template <DType T, int EPI>
 static void launch_gemm_lds(const GemmArgs &a, hipStream_t s, const LaunchEvents &ev) {
     // up to 256 rows (the drafter update): one token tile of 256 rows, so each weight block is read
     // by one workgroup (update forward 94 -> 91 us at the 7B head, full-ring update 0.450 ->
-    // 0.409 ms); prefill blocks: 128 rows x 256 features
-    if (a.M <= 256) launch_gemm_lds_shape<T, EPI, 4>(a, s, ev);
-    else launch_gemm_lds_shape<T, EPI, 2>(a, s, ev);
+    // 0.409 ms), and, the grid being one workgroup per compute unit, ring stages of two chunks
+    // (144 KiB, one barrier per two chunks: 91 -> 89 us); prefill blocks: 128 rows x 256
+    // features, one-chunk stages (72 KiB), two workgroups per compute unit
+    const int KT = a.K / ((T == DType::BF16) ? 32 : 16);
+    if (a.M <= 256 && KT % 2 == 0) launch_gemm_lds_shape<T, EPI, 4, 2>(a, s, ev);
+    else if (a.M <= 256) launch_gemm_lds_shape<T, EPI, 4, 1>(a, s, ev);
+    else launch_gemm_lds_shape<T, EPI, 2, 1>(a, s, ev);
 }
 
 template <DType T>
