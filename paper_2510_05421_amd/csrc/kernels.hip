@@ -1658,7 +1658,7 @@ __global__ void upd_counts_kernel(const int8_t *r, const int8_t *fresh, int n, f
 
 // Row i: p = softmax(z), q = softmax(l/tau); KL, entropy, log p(a); then overwrite z with
 // g = alpha p (log p - log q - KL) + beta (p - e_a) + eps p (log p + H).  One 1024-thread
-// workgroup per row; the maxima and normalisers come from one pass with a running rescale.
+// workgroup per row; the row maxima first, then the normalisers as sums of exp(x - max).
 __device__ __forceinline__ float block_sum1024(float v, float *lds16) {
     v = wave_sum(v);
     const int w = threadIdx.x >> 6;
@@ -1683,8 +1683,10 @@ __device__ __forceinline__ float block_max1024(float v, float *lds16) {
 }
 
 // The row kernel (see above): thread t takes entries v = t + 1024 e in order; the first NE of them
-// (e < NE) are read once into registers and serve all three passes, any beyond 1024 NE are read
-// from memory in each pass, with the same arithmetic (7B ring of 256 rows: 54.8 -> 36.5 us).
+// (e < NE) are read once into registers and serve every pass, any beyond 1024 NE are read from
+// memory in each pass (7B ring of 256 rows: 54.8 -> 36.5 us).  The maxima come before the sums,
+// so no running rescale and no branch per entry, and the exponentials (arguments <= 0) take the
+// hardware exp2 (36.5 -> 23.1 us); the gradients stay within a few 1e-6 of the oracle.
 template <int NE>
 __global__ void __launch_bounds__(1024) upd_rows_kernel(UpdateArgs u, const float *counts) {
     __shared__ float red[16];
@@ -1700,34 +1702,39 @@ __global__ void __launch_bounds__(1024) upd_rows_kernel(UpdateArgs u, const floa
         zr[e] = z[v];
         qr[e] = lg[v] * itau;
     }
-    // per-thread running maximum and rescaled sum of both distributions
-    float mz = -INFINITY, mq = -INFINITY, sz = 0.f, sq = 0.f;
-    auto online = [&](float a, float b) {
-        if (a > mz) {
-            sz = sz * expf(mz - a) + 1.f;
-            mz = a;
-        } else {
-            sz += expf(a - mz);
-        }
-        if (b > mq) {
-            sq = sq * expf(mq - b) + 1.f;
-            mq = b;
-        } else {
-            sq += expf(b - mq);
-        }
-    };
+    // both distributions' maxima over the row, then their sums of exp(x - max)
+    float mz = -INFINITY, mq = -INFINITY;
 #pragma unroll
     for (int e = 0; e < NE; ++e)
-        if ((int)threadIdx.x + 1024 * e < u.V) online(zr[e], qr[e]);
-    for (int v = tail; v < u.V; v += 1024) online(z[v], lg[v] * itau);
+        if ((int)threadIdx.x + 1024 * e < u.V) {
+            mz = fmaxf(mz, zr[e]);
+            mq = fmaxf(mq, qr[e]);
+        }
+    for (int v = tail; v < u.V; v += 1024) {
+        mz = fmaxf(mz, z[v]);
+        mq = fmaxf(mq, lg[v] * itau);
+    }
     const float Mz = block_max1024(mz, red), Mq = block_max1024(mq, red);
-    sz = block_sum1024(mz == -INFINITY ? 0.f : sz * expf(mz - Mz), red);
-    sq = block_sum1024(mq == -INFINITY ? 0.f : sq * expf(mq - Mq), red);
+    float sz = 0.f, sq = 0.f;
+    if (Mz > -INFINITY && Mq > -INFINITY) {  // uniform; logits are finite
+#pragma unroll
+        for (int e = 0; e < NE; ++e)
+            if ((int)threadIdx.x + 1024 * e < u.V) {
+                sz += exp_fast(zr[e] - Mz);
+                sq += exp_fast(qr[e] - Mq);
+            }
+        for (int v = tail; v < u.V; v += 1024) {
+            sz += exp_fast(z[v] - Mz);
+            sq += exp_fast(lg[v] * itau - Mq);
+        }
+    }
+    sz = block_sum1024(sz, red);
+    sq = block_sum1024(sq, red);
     const float lz = Mz + logf(sz), lq = Mq + logf(sq);
     float kl = 0.f, ent = 0.f;
     auto klent = [&](float zv, float qv) {
         const float lp = zv - lz, lqv = qv - lq;
-        const float p = expf(lp);
+        const float p = exp_fast(lp);
         kl += p * (lp - lqv);
         ent -= p * lp;
     };
@@ -1747,7 +1754,7 @@ __global__ void __launch_bounds__(1024) upd_rows_kernel(UpdateArgs u, const floa
     __syncthreads();  // every thread has read z[ai] before it is overwritten
     auto grad = [&](int v, float zv, float qv) {
         const float lp = zv - lz, lqv = qv - lq;
-        const float p = expf(lp);
+        const float p = exp_fast(lp);
         z[v] = alpha * p * (lp - lqv - kl) + beta * (p - (v == ai ? 1.f : 0.f)) + eps * p * (lp + ent);
     };
 #pragma unroll
