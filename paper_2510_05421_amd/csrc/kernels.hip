@@ -1805,14 +1805,25 @@ __global__ void upd_loss_kernel(UpdateArgs u, const float *counts) {
 // Sums p[0..15] over the 64 lanes of the wave, all sixteen at once: four halving steps each hand
 // half of the carried values to the lane 32, 16, 8 apart and then to the mirror lane of the
 // 8-lane half row (lane ^ 7), keeping the other half; two plain steps add within the quad.  Lane l
-// returns the total of value l >> 2.  The tree is fixed, so the sums are deterministic.
+// returns the total of value l >> 2.  The tree is fixed, so the sums are deterministic.  The first
+// two steps use v_permlane32_swap / v_permlane16_swap: swapping the upper half-wave (odd rows) of
+// value k with the lower half-wave (even rows) of value k + 8 (k + 4) leaves each lane its own and
+// its partner's share of the value it keeps, in two registers that one add combines.
+__device__ __forceinline__ float swap_sum32(float lo, float hi) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(lo), __float_as_uint(hi), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float swap_sum16(float lo, float hi) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(lo), __float_as_uint(hi), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
 __device__ __forceinline__ float transpose_sum16(const float (&p)[16], int lane) {
-    const bool h32 = lane & 32, h16 = lane & 16, h8 = lane & 8, h4 = lane & 4;
+    const bool h8 = lane & 8, h4 = lane & 4;
     float q[8], r[4], t[2];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) q[k] = (h32 ? p[k + 8] : p[k]) + __shfl_xor(h32 ? p[k] : p[k + 8], 32);
+    for (int k = 0; k < 8; ++k) q[k] = swap_sum32(p[k], p[k + 8]);  // lanes < 32: value k, else k + 8
 #pragma unroll
-    for (int k = 0; k < 4; ++k) r[k] = (h16 ? q[k + 4] : q[k]) + __shfl_xor(h16 ? q[k] : q[k + 4], 16);
+    for (int k = 0; k < 4; ++k) r[k] = swap_sum16(q[k], q[k + 4]);  // even rows: k, odd rows: k + 4
 #pragma unroll
     for (int k = 0; k < 2; ++k) t[k] = (h8 ? r[k + 2] : r[k]) + dpp_f32<0x128>(h8 ? r[k] : r[k + 2]);  // row_ror 8
     float v = (h4 ? t[1] : t[0]) + dpp_f32<0x141>(h4 ? t[0] : t[1]);  // half-row mirror
