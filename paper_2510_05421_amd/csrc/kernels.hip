@@ -329,44 +329,41 @@ typedef __attribute__((address_space(3))) uint8_t lds_u8;
 typedef unsigned v4u32 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ uint4 as_uint4(v4u32 v) { return uint4{v.x, v.y, v.z, v.w}; }
 
-// The wave's fragments of one chunk, read from LDS and awaited: 4 activation groups at xa and NW
+// The wave's fragments of one chunk, read from LDS and awaited: NX activation groups at xa and NW
 // weight tiles at wa (byte addresses; fragment i is i KiB further).  The reads and the wait are
 // one asm statement, so nothing can use (or copy) a register before its read has completed; the
 // outputs are early-clobber so none of them overwrites an address a later read still needs.
-template <int NW>
-__device__ __forceinline__ void lds_fragments(uint32_t xa, uint32_t wa, uint4 (&xf)[4], uint4 (&wf)[NW]) {
-    v4u32 x0, x1, x2, x3, w0, w1, w2, w3;
-    if constexpr (NW == 8) {
-        v4u32 w4, w5, w6, w7;
-        asm volatile(
-            "ds_read_b128 %0, %12 offset:0\n\tds_read_b128 %1, %12 offset:1024\n\t"
-            "ds_read_b128 %2, %12 offset:2048\n\tds_read_b128 %3, %12 offset:3072\n\t"
-            "ds_read_b128 %4, %13 offset:0\n\tds_read_b128 %5, %13 offset:1024\n\t"
-            "ds_read_b128 %6, %13 offset:2048\n\tds_read_b128 %7, %13 offset:3072\n\t"
-            "ds_read_b128 %8, %13 offset:4096\n\tds_read_b128 %9, %13 offset:5120\n\t"
-            "ds_read_b128 %10, %13 offset:6144\n\tds_read_b128 %11, %13 offset:7168\n\t"
-            "s_waitcnt lgkmcnt(0)"
-            : "=&v"(x0), "=&v"(x1), "=&v"(x2), "=&v"(x3), "=&v"(w0), "=&v"(w1), "=&v"(w2), "=&v"(w3),
-              "=&v"(w4), "=&v"(w5), "=&v"(w6), "=&v"(w7)
-            : "v"(xa), "v"(wa));
-        wf[4] = as_uint4(w4);
-        wf[5] = as_uint4(w5);
-        wf[6] = as_uint4(w6);
-        wf[7] = as_uint4(w7);
+#define DVI_RD(o, a, off) "ds_read_b128 %" #o ", %" #a " offset:" #off "\n\t"
+template <int NX, int NW>
+__device__ __forceinline__ void lds_fragments(uint32_t xa, uint32_t wa, uint4 (&xf)[NX], uint4 (&wf)[NW]) {
+    v4u32 r[NX + NW];
+    if constexpr (NX == 4 && NW == 4) {
+        asm volatile(DVI_RD(0, 8, 0) DVI_RD(1, 8, 1024) DVI_RD(2, 8, 2048) DVI_RD(3, 8, 3072)
+                     DVI_RD(4, 9, 0) DVI_RD(5, 9, 1024) DVI_RD(6, 9, 2048) DVI_RD(7, 9, 3072) "s_waitcnt lgkmcnt(0)"
+                     : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3]), "=&v"(r[4]), "=&v"(r[5]), "=&v"(r[6]),
+                       "=&v"(r[7])
+                     : "v"(xa), "v"(wa));
+    } else if constexpr (NX == 4 && NW == 8) {
+        asm volatile(DVI_RD(0, 12, 0) DVI_RD(1, 12, 1024) DVI_RD(2, 12, 2048) DVI_RD(3, 12, 3072)
+                     DVI_RD(4, 13, 0) DVI_RD(5, 13, 1024) DVI_RD(6, 13, 2048) DVI_RD(7, 13, 3072)
+                     DVI_RD(8, 13, 4096) DVI_RD(9, 13, 5120) DVI_RD(10, 13, 6144) DVI_RD(11, 13, 7168)
+                     "s_waitcnt lgkmcnt(0)"
+                     : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3]), "=&v"(r[4]), "=&v"(r[5]), "=&v"(r[6]),
+                       "=&v"(r[7]), "=&v"(r[8]), "=&v"(r[9]), "=&v"(r[10]), "=&v"(r[11])
+                     : "v"(xa), "v"(wa));
     } else {
-        static_assert(NW == 4, "4 or 8 weight tiles per wave");
-        asm volatile(
-            "ds_read_b128 %0, %8 offset:0\n\tds_read_b128 %1, %8 offset:1024\n\t"
-            "ds_read_b128 %2, %8 offset:2048\n\tds_read_b128 %3, %8 offset:3072\n\t"
-            "ds_read_b128 %4, %9 offset:0\n\tds_read_b128 %5, %9 offset:1024\n\t"
-            "ds_read_b128 %6, %9 offset:2048\n\tds_read_b128 %7, %9 offset:3072\n\t"
-            "s_waitcnt lgkmcnt(0)"
-            : "=&v"(x0), "=&v"(x1), "=&v"(x2), "=&v"(x3), "=&v"(w0), "=&v"(w1), "=&v"(w2), "=&v"(w3)
-            : "v"(xa), "v"(wa));
+        static_assert(NX == 2 && NW == 4, "fragment counts");
+        asm volatile(DVI_RD(0, 6, 0) DVI_RD(1, 6, 1024) DVI_RD(2, 7, 0) DVI_RD(3, 7, 1024) DVI_RD(4, 7, 2048)
+                     DVI_RD(5, 7, 3072) "s_waitcnt lgkmcnt(0)"
+                     : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3]), "=&v"(r[4]), "=&v"(r[5])
+                     : "v"(xa), "v"(wa));
     }
-    xf[0] = as_uint4(x0); xf[1] = as_uint4(x1); xf[2] = as_uint4(x2); xf[3] = as_uint4(x3);
-    wf[0] = as_uint4(w0); wf[1] = as_uint4(w1); wf[2] = as_uint4(w2); wf[3] = as_uint4(w3);
+#pragma unroll
+    for (int q = 0; q < NX; ++q) xf[q] = as_uint4(r[q]);
+#pragma unroll
+    for (int t = 0; t < NW; ++t) wf[t] = as_uint4(r[NX + t]);
 }
+#undef DVI_RD
 
 // Logits epilogue of the large-M GEMM (the drafter update's 65-256 replay rows): for every
 // output z = sc * acc + gamma * sum_c A_s[n][c] u[m][c], the LoRA sum taken over the rank in
@@ -375,8 +372,8 @@ __device__ __forceinline__ void lds_fragments(uint32_t xa, uint32_t wa, uint4 (&
 // so each lane reads its factors from LDS instead of gathering them from memory, and the lane's
 // four consecutive logits of a row group leave in one 16-byte store.  Writes logits only: no
 // argmax partials, no sampling (the update asks for neither).
-template <int WV, int XF, int WF, int NW>
-__device__ __forceinline__ void lds_logits_epilogue(const GemmArgs &a, const f32x4 (&acc)[NW][4], float *smem,
+template <int WV, int XF, int WF, int NW, int GPW>
+__device__ __forceinline__ void lds_logits_epilogue(const GemmArgs &a, const f32x4 (&acc)[NW][GPW], float *smem,
                                                     int g0, int t0, int wy, int wx) {
     constexpr int RS = 32, LD = RS + 1;  // rank columns per pass; padded row stride in floats
     const int lane = threadIdx.x & 63, G4 = lane >> 4;
@@ -384,11 +381,11 @@ __device__ __forceinline__ void lds_logits_epilogue(const GemmArgs &a, const f32
     const int m_base = 16 * g0, n_base = 16 * t0;
     float *us = smem;                // [16 XF rows][LD]
     float *as = smem + 16 * XF * LD;  // [16 WF rows][LD]
-    float sacc[NW][4][4];
+    float sacc[NW][GPW][4];
 #pragma unroll
     for (int t = 0; t < NW; ++t)
 #pragma unroll
-        for (int g = 0; g < 4; ++g)
+        for (int g = 0; g < GPW; ++g)
 #pragma unroll
             for (int j = 0; j < 4; ++j) sacc[t][g][j] = 0.f;
     const int r = a.lora_A != nullptr ? a.r : 0;
@@ -405,16 +402,16 @@ __device__ __forceinline__ void lds_logits_epilogue(const GemmArgs &a, const f32
         }
         __syncthreads();
         for (int c = 0; c < rc; ++c) {
-            float uv[4];
+            float uv[GPW];
 #pragma unroll
-            for (int g = 0; g < 4; ++g) uv[g] = us[(16 * (4 * wy + g) + (lane & 15)) * LD + c];
+            for (int g = 0; g < GPW; ++g) uv[g] = us[(16 * (GPW * wy + g) + (lane & 15)) * LD + c];
 #pragma unroll
             for (int t = 0; t < NW; ++t)
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
                     const float av = as[(16 * (NW * wx + t) + 4 * G4 + j) * LD + c];
 #pragma unroll
-                    for (int g = 0; g < 4; ++g) sacc[t][g][j] += av * uv[g];
+                    for (int g = 0; g < GPW; ++g) sacc[t][g][j] += av * uv[g];
                 }
         }
     }
@@ -422,8 +419,8 @@ __device__ __forceinline__ void lds_logits_epilogue(const GemmArgs &a, const f32
     for (int t = 0; t < NW; ++t) {
         const int nt = t0 + NW * wx + t;
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-            const int m = m_base + 16 * (4 * wy + g) + (lane & 15);
+        for (int g = 0; g < GPW; ++g) {
+            const int m = m_base + 16 * (GPW * wy + g) + (lane & 15);
             if (nt < NT && m < a.M) {
                 const float sc = a.ss_in != nullptr ? a.sinv_rows[m] : 1.0f;
                 float y[4];
@@ -438,16 +435,16 @@ __device__ __forceinline__ void lds_logits_epilogue(const GemmArgs &a, const f32
     }
 }
 
-// WV waves as WY (tokens) x WX (features), every wave tile 64 tokens x 16 NW features.  A chunk
-// has FR = 24 fragments: XF = 4 WY activation groups and WF = FR - XF weight tiles.  A ring stage
-// holds CPS consecutive chunks (KT a multiple of CPS), so the workgroup meets at one barrier per
-// CPS chunks.
-template <DType T, int EPI, int WV, int WY, int CPS>
+// WV waves as WY (tokens) x WX (features), every wave tile 16 GPW tokens x 16 NW features.  A
+// chunk has FR = 24 fragments: XF = GPW WY activation groups and WF = FR - XF weight tiles.  A ring
+// stage holds CPS consecutive chunks (KT a multiple of CPS), so the workgroup meets at one barrier
+// per CPS chunks; each wave copies PS = CPS FR / WV of a stage's fragments.
+template <DType T, int EPI, int WV, int WY, int CPS, int GPW>
 __global__ void __launch_bounds__(64 * WV) gemm_lds_kernel(GemmArgs a, int n_tok_tiles, int n_tiles_total) {
-    constexpr int NS = kLdsStages, FR = 24, PER = FR / WV;  // stages, fragments per chunk, per wave
-    constexpr int XF = 4 * WY, WF = FR - XF;                // activation groups, weight tiles per chunk
-    constexpr int WX = WV / WY, NW = WF / WX;               // waves across the features; tiles per wave
-    static_assert(WX * WY == WV && NW * WX == WF && PER * WV == FR, "workgroup shape");
+    constexpr int NS = kLdsStages, FR = 24, PS = CPS * FR / WV;  // stages, fragments per chunk, per wave and stage
+    constexpr int XF = GPW * WY, WF = FR - XF;                     // activation groups, weight tiles per chunk
+    constexpr int WX = WV / WY, NW = WF / WX;                      // waves across the features; tiles per wave
+    static_assert(WX * WY == WV && NW * WX == WF && PS * WV == CPS * FR, "workgroup shape");
     constexpr uint32_t kChunk = FR * 1024, kStage = CPS * kChunk;
     __shared__ __align__(1024) uint4 ring[NS][CPS * FR][64];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -460,35 +457,36 @@ __global__ void __launch_bounds__(64 * WV) gemm_lds_kernel(GemmArgs a, int n_tok
     const int tl = (blockIdx.x & 7) * per + j;
     if (j >= per || tl >= n_tiles_total) return;  // uniform across the workgroup (before any barrier)
     const int g0 = (tl % n_tok_tiles) * XF, t0 = (tl / n_tok_tiles) * WF;
-    // the fragments this wave loads into every stage: f = PER * wave + i; f < XF: activation group
-    // g0 + f, else weight tile t0 + f - XF (clamped into range)
-    const uint4 *src[PER];
+    // the stage fragments this wave copies: f = PS * wave + i is fragment fr = f % FR of the
+    // stage's chunk f / FR; fr < XF: activation group g0 + fr, else weight tile t0 + fr - XF
+    // (clamped into range).  Stage layout: fragment f at f KiB.
+    const uint4 *src[PS];
+    int coff[PS];
 #pragma unroll
-    for (int i = 0; i < PER; ++i) {
-        const int f = PER * wave + i;
-        src[i] = (f < XF ? (const uint4 *)a.X + (size_t)min(g0 + f, NG - 1) * KT * 64
-                         : (const uint4 *)a.W + (size_t)min(t0 + f - XF, NT - 1) * KT * 64) + lane;
+    for (int i = 0; i < PS; ++i) {
+        const int f = PS * wave + i, fr = f % FR;
+        coff[i] = f / FR;
+        src[i] = (fr < XF ? (const uint4 *)a.X + (size_t)min(g0 + fr, NG - 1) * KT * 64
+                          : (const uint4 *)a.W + (size_t)min(t0 + fr - XF, NT - 1) * KT * 64) + lane;
     }
     lds_u8 *const ring0 = (lds_u8 *)&ring[0][0][0];
     // stage st <- chunks CPS k .. CPS k + CPS - 1
     auto issue = [&](int st, int k) {
 #pragma unroll
-        for (int cc = 0; cc < CPS; ++cc)
-#pragma unroll
-            for (int i = 0; i < PER; ++i)
-                __builtin_amdgcn_global_load_lds((const void *)(src[i] + (size_t)(CPS * k + cc) * 64),
-                                                 (__attribute__((address_space(3))) void *)(ring0 + st * kStage + cc * kChunk +
-                                                                                             (PER * wave + i) * 1024),
-                                                 16, 0, 0);
+        for (int i = 0; i < PS; ++i)
+            __builtin_amdgcn_global_load_lds((const void *)(src[i] + (size_t)(CPS * k + coff[i]) * 64),
+                                             (__attribute__((address_space(3))) void *)(ring0 + st * kStage +
+                                                                                         (PS * wave + i) * 1024),
+                                             16, 0, 0);
     };
     // this lane's LDS byte address in fragment 0 of stage 0; fragment f of stage st is f KiB and
     // st stages further
     const uint32_t lbase = (uint32_t)(uintptr_t)ring0 + 16 * lane;
-    f32x4 acc[NW][4];
+    f32x4 acc[NW][GPW];
 #pragma unroll
     for (int t = 0; t < NW; ++t)
 #pragma unroll
-        for (int g = 0; g < 4; ++g) acc[t][g] = (f32x4){0.f, 0.f, 0.f, 0.f};
+        for (int g = 0; g < GPW; ++g) acc[t][g] = (f32x4){0.f, 0.f, 0.f, 0.f};
     const int KS = KT / CPS;  // stages of the K loop
 #pragma unroll
     for (int st = 0; st < NS - 1; ++st)
@@ -497,10 +495,10 @@ __global__ void __launch_bounds__(64 * WV) gemm_lds_kernel(GemmArgs a, int n_tok
         // stage k's loads are done once at most min(NS - 2, KS - 1 - k) later stages are in flight
         const int later = min(NS - 2, KS - 1 - k);
         static_assert(NS - 2 <= 4, "wait cases");
-        if (later >= 4) wait_vmcnt<4 * PER * CPS>();
-        else if (later == 3) wait_vmcnt<3 * PER * CPS>();
-        else if (later == 2) wait_vmcnt<2 * PER * CPS>();
-        else if (later == 1) wait_vmcnt<PER * CPS>();
+        if (later >= 4) wait_vmcnt<4 * PS>();
+        else if (later == 3) wait_vmcnt<3 * PS>();
+        else if (later == 2) wait_vmcnt<2 * PS>();
+        else if (later == 1) wait_vmcnt<PS>();
         else wait_vmcnt<0>();
         // every wave's fragments of stage k are in LDS, and every wave is done with the stage the
         // next issue overwrites (its LDS reads of stage k - 1 completed before its MFMAs)
@@ -509,42 +507,45 @@ __global__ void __launch_bounds__(64 * WV) gemm_lds_kernel(GemmArgs a, int n_tok
 #pragma unroll
         for (int cc = 0; cc < CPS; ++cc) {
             const uint32_t sb = lbase + (uint32_t)(k % NS) * kStage + cc * kChunk;
-            uint4 xf[4], wf[NW];
-            lds_fragments<NW>(sb + 4 * wy * 1024, sb + (XF + NW * wx) * 1024, xf, wf);
+            uint4 xf[GPW], wf[NW];
+            lds_fragments<GPW, NW>(sb + GPW * wy * 1024, sb + (XF + NW * wx) * 1024, xf, wf);
 #pragma unroll
             for (int t = 0; t < NW; ++t)
 #pragma unroll
-                for (int g = 0; g < 4; ++g) acc[t][g] = St<T>::mma(wf[t], xf[g], acc[t][g]);
+                for (int g = 0; g < GPW; ++g) acc[t][g] = St<T>::mma(wf[t], xf[g], acc[t][g]);
         }
     }
     if constexpr (EPI == EPI_LOGITS) {
-        lds_logits_epilogue<WV, XF, WF, NW>(a, acc, (float *)&ring[0][0][0], g0, t0, wy, wx);
+        lds_logits_epilogue<WV, XF, WF, NW, GPW>(a, acc, (float *)&ring[0][0][0], g0, t0, wy, wx);
         return;
-    }
-    const int gw = g0 + 4 * wy;
-    if (gw >= NG) return;  // uniform across the wave
-    const int m0 = 16 * gw;
+    } else {
+        static_assert(GPW == 4, "the decode epilogues take four row groups");
+        const int gw = g0 + 4 * wy;
+        if (gw >= NG) return;  // uniform across the wave
+        const int m0 = 16 * gw;
 #pragma unroll
-    for (int t = 0; t < NW; ++t) {
-        const int nt = t0 + NW * wx + t;
-        if (nt < NT) {  // uniform; a guard, not a break, so the loop unrolls and acc stays in registers
-            EpiOperands<4> pre;
-            epilogue_prefetch<4, EPI>(a, nt, pre, m0);
-            epilogue_prefetch_rope<4, EPI>(a, nt, pre);
-            gemm_epilogue<T, 4, EPI>(a, nt, acc[t], a.sinv_rows + m0, pre, m0);
+        for (int t = 0; t < NW; ++t) {
+            const int nt = t0 + NW * wx + t;
+            if (nt < NT) {  // uniform; a guard, not a break, so the loop unrolls and acc stays in registers
+                EpiOperands<4> pre;
+                epilogue_prefetch<4, EPI>(a, nt, pre, m0);
+                epilogue_prefetch_rope<4, EPI>(a, nt, pre);
+                gemm_epilogue<T, 4, EPI>(a, nt, acc[t], a.sinv_rows + m0, pre, m0);
+            }
         }
     }
 }
 
-template <DType T, int EPI, int WY, int CPS>
+template <DType T, int EPI, int WV, int WY, int CPS, int GPW>
 static void launch_gemm_lds_shape(const GemmArgs &a, hipStream_t s, const LaunchEvents &ev) {
-    constexpr int WV = kLdsWaves, XF = 4 * WY, WF = 24 - XF;
+    constexpr int XF = GPW * WY, WF = 24 - XF;
     const int tok = (a.M + 16 * XF - 1) / (16 * XF), blk = (a.N / 16 + WF - 1) / WF, total = tok * blk;
     const int grid = 8 * ((total + 7) / 8);
     if (ev.start || ev.stop)
-        hipExtLaunchKernelGGL(gemm_lds_kernel<T, EPI, WV, WY, CPS>, dim3(grid), dim3(64 * WV), 0, s, ev.start, ev.stop, 0, a, tok, total);
+        hipExtLaunchKernelGGL(gemm_lds_kernel<T, EPI, WV, WY, CPS, GPW>, dim3(grid), dim3(64 * WV), 0, s, ev.start, ev.stop, 0, a,
+                              tok, total);
     else
-        gemm_lds_kernel<T, EPI, WV, WY, CPS><<<grid, 64 * WV, 0, s>>>(a, tok, total);
+        gemm_lds_kernel<T, EPI, WV, WY, CPS, GPW><<<grid, 64 * WV, 0, s>>>(a, tok, total);
 }
 
 template <DType T, int EPI>
@@ -552,12 +553,18 @@ static void launch_gemm_lds(const GemmArgs &a, hipStream_t s, const LaunchEvents
     // up to 256 rows (the drafter update): one token tile of 256 rows, so each weight block is read
     // by one workgroup (update forward 94 -> 91 us at the 7B head, full-ring update 0.450 ->
     // 0.409 ms), and, the grid being one workgroup per compute unit, ring stages of two chunks
-    // (144 KiB, one barrier per two chunks: 91 -> 89 us); prefill blocks: 128 rows x 256
-    // features, one-chunk stages (72 KiB), two workgroups per compute unit
+    // (144 KiB, one barrier per two chunks: 91 -> 89 us).  The update's logits take 16 waves of
+    // 32 x 64 tiles (four waves per SIMD in 116 registers instead of two: 89 -> 85 us).  Prefill
+    // blocks: 128 rows x 256 features, one-chunk stages (72 KiB), two workgroups per compute unit.
     const int KT = a.K / ((T == DType::BF16) ? 32 : 16);
-    if (a.M <= 256 && KT % 2 == 0) launch_gemm_lds_shape<T, EPI, 4, 2>(a, s, ev);
-    else if (a.M <= 256) launch_gemm_lds_shape<T, EPI, 4, 1>(a, s, ev);
-    else launch_gemm_lds_shape<T, EPI, 2, 1>(a, s, ev);
+    if constexpr (EPI == EPI_LOGITS) {
+        if (KT % 2 == 0) launch_gemm_lds_shape<T, EPI, 16, 8, 2, 2>(a, s, ev);
+        else launch_gemm_lds_shape<T, EPI, kLdsWaves, 4, 1, 4>(a, s, ev);
+    } else {
+        if (a.M <= 256 && KT % 2 == 0) launch_gemm_lds_shape<T, EPI, kLdsWaves, 4, 2, 4>(a, s, ev);
+        else if (a.M <= 256) launch_gemm_lds_shape<T, EPI, kLdsWaves, 4, 1, 4>(a, s, ev);
+        else launch_gemm_lds_shape<T, EPI, kLdsWaves, 2, 1, 4>(a, s, ev);
+    }
 }
 
 template <DType T>
