@@ -440,7 +440,7 @@ __device__ __forceinline__ void lds_logits_epilogue(const GemmArgs &a, const f32
 // stage holds CPS consecutive chunks (KT a multiple of CPS), so the workgroup meets at one barrier
 // per CPS chunks; each wave copies PS = CPS FR / WV of a stage's fragments.
 template <DType T, int EPI, int WV, int WY, int CPS, int GPW>
-__global__ void __launch_bounds__(64 * WV) gemm_lds_kernel(GemmArgs a, int n_tok_tiles, int n_tiles_total) {
+__global__ void __launch_bounds__(64 * WV, (WV == 8 && CPS == 1 && EPI == EPI_QKV) ? 4 : 1) gemm_lds_kernel(GemmArgs a, int n_tok_tiles, int n_tiles_total) {
     constexpr int NS = kLdsStages, FR = 24, PS = CPS * FR / WV;  // stages, fragments per chunk, per wave and stage
     constexpr int XF = GPW * WY, WF = FR - XF;                     // activation groups, weight tiles per chunk
     constexpr int WX = WV / WY, NW = WF / WX;                      // waves across the features; tiles per wave
@@ -464,8 +464,8 @@ __global__ void __launch_bounds__(64 * WV) gemm_lds_kernel(GemmArgs a, int n_tok
     int coff[PS];
 #pragma unroll
     for (int i = 0; i < PS; ++i) {
-        const int f = PS * wave + i, fr = f % FR;
-        coff[i] = f / FR;
+        const int f = PS * wave + i, fr = CPS == 1 ? f : f % FR;  // with one chunk, f < FR already
+        coff[i] = CPS == 1 ? 0 : f / FR;
         src[i] = (fr < XF ? (const uint4 *)a.X + (size_t)min(g0 + fr, NG - 1) * KT * 64
                           : (const uint4 *)a.W + (size_t)min(t0 + fr - XF, NT - 1) * KT * 64) + lane;
     }
@@ -555,7 +555,10 @@ static void launch_gemm_lds(const GemmArgs &a, hipStream_t s, const LaunchEvents
     // 0.409 ms), and, the grid being one workgroup per compute unit, ring stages of two chunks
     // (144 KiB, one barrier per two chunks: 91 -> 89 us).  The update's logits take 16 waves of
     // 32 x 64 tiles (four waves per SIMD in 116 registers instead of two: 89 -> 85 us).  Prefill
-    // blocks: 128 rows x 256 features, one-chunk stages (72 KiB), two workgroups per compute unit.
+    // blocks: 128 rows x 256 features, one-chunk stages (72 KiB); QKV under a 128-register bound
+    // (its epilogue spills 28 bytes) so that two workgroups share a compute unit, as gate/up's
+    // 112 registers allow anyway (8 x 2048 prefill QKV 261 -> 232 us; out-proj/down lose 3% under
+    // the same bound and keep their 136).
     const int KT = a.K / ((T == DType::BF16) ? 32 : 16);
     if constexpr (EPI == EPI_LOGITS) {
         if (KT % 2 == 0) launch_gemm_lds_shape<T, EPI, 16, 8, 2, 2>(a, s, ev);
