@@ -519,18 +519,17 @@ __global__ void __launch_bounds__(64 * WV, (WV == 8 && CPS == 1 && EPI == EPI_QK
         lds_logits_epilogue<WV, XF, WF, NW, GPW>(a, acc, (float *)&ring[0][0][0], g0, t0, wy, wx);
         return;
     } else {
-        static_assert(GPW == 4, "the decode epilogues take four row groups");
-        const int gw = g0 + 4 * wy;
+        const int gw = g0 + GPW * wy;
         if (gw >= NG) return;  // uniform across the wave
         const int m0 = 16 * gw;
 #pragma unroll
         for (int t = 0; t < NW; ++t) {
             const int nt = t0 + NW * wx + t;
             if (nt < NT) {  // uniform; a guard, not a break, so the loop unrolls and acc stays in registers
-                EpiOperands<4> pre;
-                epilogue_prefetch<4, EPI>(a, nt, pre, m0);
-                epilogue_prefetch_rope<4, EPI>(a, nt, pre);
-                gemm_epilogue<T, 4, EPI>(a, nt, acc[t], a.sinv_rows + m0, pre, m0);
+                EpiOperands<GPW> pre;
+                epilogue_prefetch<GPW, EPI>(a, nt, pre, m0);
+                epilogue_prefetch_rope<GPW, EPI>(a, nt, pre);
+                gemm_epilogue<T, GPW, EPI>(a, nt, acc[t], a.sinv_rows + m0, pre, m0);
             }
         }
     }
@@ -557,8 +556,10 @@ static void launch_gemm_lds(const GemmArgs &a, hipStream_t s, const LaunchEvents
     // 32 x 64 tiles (four waves per SIMD in 116 registers instead of two: 89 -> 85 us).  Prefill
     // blocks: 128 rows x 256 features, one-chunk stages (72 KiB); QKV under a 128-register bound
     // (its epilogue spills 28 bytes) so that two workgroups share a compute unit, as gate/up's
-    // 112 registers allow anyway (8 x 2048 prefill QKV 261 -> 232 us; out-proj/down lose 3% under
-    // the same bound and keep their 136).
+    // 112 registers allow anyway (8 x 2048 prefill QKV 261 -> 232 us).  Out-proj/down (136
+    // registers, one workgroup per compute unit) take the update's arrangement instead: 16 waves
+    // of 32 x 64 tiles over two-chunk stages, four waves per SIMD (149 -> 137-141 us); gate/up and
+    // QKV lose with it (347 -> 395, 232 -> 245 us).
     const int KT = a.K / ((T == DType::BF16) ? 32 : 16);
     if constexpr (EPI == EPI_LOGITS) {
         if (KT % 2 == 0) launch_gemm_lds_shape<T, EPI, 16, 8, 2, 2>(a, s, ev);
@@ -566,6 +567,7 @@ static void launch_gemm_lds(const GemmArgs &a, hipStream_t s, const LaunchEvents
     } else {
         if (a.M <= 256 && KT % 2 == 0) launch_gemm_lds_shape<T, EPI, kLdsWaves, 4, 2, 4>(a, s, ev);
         else if (a.M <= 256) launch_gemm_lds_shape<T, EPI, kLdsWaves, 4, 1, 4>(a, s, ev);
+        else if (EPI == EPI_RESID && KT % 2 == 0) launch_gemm_lds_shape<T, EPI, 16, 4, 2, 2>(a, s, ev);
         else launch_gemm_lds_shape<T, EPI, kLdsWaves, 2, 1, 4>(a, s, ev);
     }
 }
