@@ -216,13 +216,15 @@ def test_buffer_rows_hold_the_verify_logits_and_normed_states():
 @pytest.mark.parametrize("name,n_rows,r,vocab", [("tiny", 48, 16, None), ("tiny", 100, 16, None), ("tiny", 300, 16, None),
                                                 ("1b_L4", 200, 16, None), ("1b_L4", 256, 16, None),
                                                 ("tiny", 100, 20, None), ("1b_L4", 200, 40, None),
-                                                ("tiny", 300, 64, None), ("tiny", 100, 16, 4112)])
+                                                ("tiny", 300, 64, None), ("tiny", 100, 16, 4112),
+                                                ("tiny", 64, 16, 33024)])
 def test_drafter_update_gradients_match_oracle(name, n_rows, r, vocab):
     """Row counts cover the update GEMM's 4-, 8- and 16-group variants and more rows than one
     launch takes (300 > 256).  Ranks other than 16 take the large-M logits epilogue through one
     partial pass over the rank (20), two passes (40: 32 + 8) and two full passes (64).  A
     vocabulary of 4112 = 32 * 128 + 16 leaves the gradient pass's last 128-entry block mostly
-    empty."""
+    empty; one of 33024 = 32 * 1024 + 256 sends the row kernel past the 32 entries per thread it
+    holds in registers."""
     shape = gu.SHAPES[name].replace(lora_rank=r)
     if vocab is not None:
         shape = shape.replace(vocab=vocab)
