@@ -59,8 +59,15 @@ void launch_pack(DType t, PackSrc srcs, const int32_t *prow, int N, int K, void 
 // is scaled by 1/sqrt(mean(h[m]^2) + eps), reduced from the partial sums of squares that the
 // producing epilogue wrote.  RMSNorm(h) W^T = (h*g) W^T / rms(h), so no separate pass over h.
 // ------------------------------------------------------------------------------------------
+// The gate/up shape at 33-64 tokens (up to three tiles) runs under a register bound that fits two
+// workgroups per compute unit (see the ring below).
+template <int MG, int EPI, int RT, int WMAX>
+constexpr bool gemm_two_per_cu() {
+    return MG >= 3 && WMAX == 8 && EPI == EPI_SWIGLU && RT <= 3;
+}
+
 template <DType T, int MG, int EPI, int RT, int WMAX>
-__global__ void __launch_bounds__(64 * WMAX, (MG >= 3 && WMAX == 8 && EPI == EPI_SWIGLU && RT <= 3) ? 4 : 1) gemm_kernel(GemmArgs a) {
+__global__ void __launch_bounds__(64 * WMAX, (gemm_two_per_cu<MG, EPI, RT, WMAX>() ? 4 : 1)) gemm_kernel(GemmArgs a) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
     const int nt0 = blockIdx.x * RT;
     // the last workgroup may hold fewer than RT tiles: tiles past N / 16 load nothing and store
@@ -119,7 +126,7 @@ __global__ void __launch_bounds__(64 * WMAX, (MG >= 3 && WMAX == 8 && EPI == EPI
     // that fits two workgroups per compute unit instead of one (7B, 64 rows: 62.9 -> 52.7 us);
     // the other epilogues, and four tiles, spill under that bound (the head at 64 rows: 86 ->
     // 145 us) and keep four stages.
-    constexpr int S = (MG >= 3 && WMAX == 8 && EPI == EPI_SWIGLU && RT <= 3) ? 2 : 4;
+    constexpr int S = gemm_two_per_cu<MG, EPI, RT, WMAX>() ? 2 : 4;
     uint4 w[S][RT], x[S][MG];
     auto fetch = [&](int cb, uint4 (&wf)[RT], uint4 (&xf)[MG]) {
         const bool in = cb < c1;
@@ -150,12 +157,45 @@ __global__ void __launch_bounds__(64 * WMAX, (MG >= 3 && WMAX == 8 && EPI == EPI
     // then runs that tile's epilogue.
     __shared__ f32x4 red[RT][WMAX][64];
     __shared__ float sinv[64];
-    if (a.ss_in != nullptr)
-        for (int m = wave; m < a.M; m += nw) {
-            const float v = (m == wave && ss_early) ? inv_rms_regs<SSP>(ssv, nparts, a.K, a.eps)
-                                                    : inv_rms(a.ss_in + (size_t)m * a.ld_ss_in, nparts, a.K, a.eps);
-            if (lane == 0) sinv[m] = v;
+    // Past 32 tokens the epilogue operands, and the partial sums of the folded norm for several
+    // rows at a time (all eight of a wave, or two under the register bound), are requested
+    // together once the ring's registers are free: a row at a time would cost a memory round trip
+    // per row (eight per wave at 64 tokens).  Same summation order as inv_rms.
+    constexpr int RPW = 8;  // rows per wave when 8 waves cover 64 tokens
+    constexpr int RB = gemm_two_per_cu<MG, EPI, RT, WMAX>() ? 2 : RPW;
+    if (!kEarly && wave < nvalid) {
+        epilogue_prefetch<MG, EPI>(a, nt0 + wave, pre);
+        epilogue_prefetch_rope<MG, EPI>(a, nt0 + wave, pre);
+    }
+    if (a.ss_in != nullptr) {
+        if (!kEarly && nw * RPW >= a.M && nparts <= 64 * SSP) {
+#pragma unroll 1
+            for (int r0 = 0; r0 < RPW; r0 += RB) {
+                float sv[RB][SSP];
+#pragma unroll
+                for (int r = 0; r < RB; ++r) {
+                    const float *src = a.ss_in + (size_t)min(wave + nw * (r0 + r), a.M - 1) * a.ld_ss_in;
+#pragma unroll
+                    for (int k = 0; k < SSP; ++k) sv[r][k] = src[min(lane + 64 * k, nparts - 1)];
+                }
+#pragma unroll
+                for (int r = 0; r < RB; ++r) {
+                    const int m = wave + nw * (r0 + r);
+                    if (m < a.M) {  // uniform across the wave
+                        const float v = inv_rms_regs<SSP>(sv[r], nparts, a.K, a.eps);
+                        if (lane == 0) sinv[m] = v;
+                    }
+                }
+            }
+        } else {
+            for (int m = wave; m < a.M; m += nw) {
+                const float v = (m == wave && ss_early)
+                                    ? inv_rms_regs<SSP>(ssv, nparts, a.K, a.eps)
+                                    : inv_rms(a.ss_in + (size_t)m * a.ld_ss_in, nparts, a.K, a.eps);
+                if (lane == 0) sinv[m] = v;
+            }
         }
+    }
     f32x4 mine[MG];
 #pragma unroll
     for (int g = 0; g < MG; ++g) {
@@ -170,13 +210,7 @@ __global__ void __launch_bounds__(64 * WMAX, (MG >= 3 && WMAX == 8 && EPI == EPI
         __syncthreads();
     }
     if (wave >= nvalid) return;
-    const int nt = nt0 + wave;
-
-    if (!kEarly) {
-        epilogue_prefetch<MG, EPI>(a, nt, pre);
-        epilogue_prefetch_rope<MG, EPI>(a, nt, pre);
-    }
-    gemm_epilogue<T, MG, EPI>(a, nt, mine, sinv, pre);
+    gemm_epilogue<T, MG, EPI>(a, nt0 + wave, mine, sinv, pre);
 }
 
 // ------------------------------------------------------------------------------------------
