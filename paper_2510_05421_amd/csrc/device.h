@@ -123,14 +123,6 @@ constexpr int CK = 64;  // attention key chunk (absolute positions)
 // Inverse RMS of one row from its per-16-column partial sums of squares: lane l adds
 // partials l, l+64, ... in order, then the wave sum, so every lane (and every workgroup that
 // asks) gets the same value.
-__device__ __forceinline__ float inv_rms(const float *ss, int nparts, int d, float eps) {
-    const int lane = threadIdx.x & 63;
-    float s = 0.f;
-    for (int t = lane; t < nparts; t += 64) s += ss[t];
-    s = wave_sum(s);
-    return 1.0f / sqrtf(s / (float)d + eps);
-}
-
 // inv_rms with the partial sums already in registers: v[k] holds ss[lane + 64k] (k < KP,
 // nparts <= 64*KP); same summation order as inv_rms.
 template <int KP>
@@ -142,6 +134,27 @@ __device__ __forceinline__ float inv_rms_regs(const float (&v)[KP], int nparts, 
         if (lane + 64 * k < nparts) s += v[k];
     s = wave_sum(s);
     return 1.0f / sqrtf(s / (float)d + eps);
+}
+
+// The same as a loop, for callers short of registers.
+__device__ __forceinline__ float inv_rms_loop(const float *ss, int nparts, int d, float eps) {
+    const int lane = threadIdx.x & 63;
+    float s = 0.f;
+    for (int t = lane; t < nparts; t += 64) s += ss[t];
+    s = wave_sum(s);
+    return 1.0f / sqrtf(s / (float)d + eps);
+}
+
+// Up to 512 partial sums (d <= 8192) are all requested before the first add (addresses clamped
+// into the row); the sum runs over lane + 64k in increasing k either way.
+__device__ __forceinline__ float inv_rms(const float *ss, int nparts, int d, float eps) {
+    const int lane = threadIdx.x & 63;
+    constexpr int KP = 8;
+    if (nparts > 64 * KP) return inv_rms_loop(ss, nparts, d, eps);
+    float v[KP];
+#pragma unroll
+    for (int k = 0; k < KP; ++k) v[k] = ss[min(lane + 64 * k, nparts - 1)];
+    return inv_rms_regs<KP>(v, nparts, d, eps);
 }
 
 // Sum of squares of 16 consecutive columns held as 4 values by each of the lanes

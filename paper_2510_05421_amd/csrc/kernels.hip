@@ -191,7 +191,7 @@ __global__ void __launch_bounds__(64 * WMAX, (gemm_two_per_cu<MG, EPI, RT, WMAX>
             for (int m = wave; m < a.M; m += nw) {
                 const float v = (m == wave && ss_early)
                                     ? inv_rms_regs<SSP>(ssv, nparts, a.K, a.eps)
-                                    : inv_rms(a.ss_in + (size_t)m * a.ld_ss_in, nparts, a.K, a.eps);
+                                    : inv_rms_loop(a.ss_in + (size_t)m * a.ld_ss_in, nparts, a.K, a.eps);
                 if (lane == 0) sinv[m] = v;
             }
         }
@@ -1538,14 +1538,27 @@ __global__ void __launch_bounds__(256) argmax_kernel(const float *pv, const int3
     const int m = blockIdx.x;
     float best = -INFINITY;
     int bidx = 0x3fffffff, bad = 0;
-    for (int t = threadIdx.x; t < ntiles; t += 256) {
-        const float v = pv[(size_t)m * ntiles + t];
-        const int code = pi[(size_t)m * ntiles + t];
-        const int idx = code & 0x3fffffff;
-        bad |= (code >> 30) & 1;
-        if (v > best || (v == best && idx < bidx)) {
-            best = v;
-            bidx = idx;
+    // Eight partials per thread are requested before the first comparison.  The winner (largest
+    // value, lowest index among equals) does not depend on the order they are compared in;
+    // slots past ntiles compare as (-inf, no index) and change nothing.
+    constexpr int U = 8;
+    for (int t0 = threadIdx.x; t0 < ntiles; t0 += 256 * U) {
+        float v[U];
+        int code[U];
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+            const int t = t0 + 256 * k;
+            v[k] = t < ntiles ? pv[(size_t)m * ntiles + t] : -INFINITY;
+            code[k] = t < ntiles ? pi[(size_t)m * ntiles + t] : 0x3fffffff;
+        }
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+            const int idx = code[k] & 0x3fffffff;
+            bad |= (code[k] >> 30) & 1;
+            if (v[k] > best || (v[k] == best && idx < bidx)) {
+                best = v[k];
+                bidx = idx;
+            }
         }
     }
 #pragma unroll
