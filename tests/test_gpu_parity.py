@@ -781,6 +781,31 @@ def test_edge_shapes_are_lossless(B, P, k):
     eng.close()
 
 
+@pytest.mark.parametrize("name,B,k", [("7b_L4", 5, 8), ("tiny", 3, 13)])
+def test_ragged_verify_blocks_are_lossless(name, B, k):
+    """Verify blocks of 33-48 rows that fill neither their last 16-row group nor every wave's
+    share of rows (5 x 8 = 40 in bf16, 3 x 13 = 39 in fp32): the decode GEMMs' three-group path,
+    with its folded-norm partial sums requested several rows at a time, gives the bits of greedy
+    decoding's one row per sequence, tokens and cache alike."""
+    shape = gu.SHAPES[name]
+    T, P = 24, 21
+    prompts = synth.make_prompts(shape.vocab, B, P, 17)
+    w = synth.make_weights(shape, 0, lora_A_std=0.05)
+    eng, _ = gu.engine(shape, max_batch=B, max_seq=P + T + k, max_k_spec=k, weights=w)
+    spec, info = eng.generate(prompts, T, k)
+    lens = eng.lengths().copy()
+    layers = (shape.split_k, shape.n_layers - 1)
+    kv = [eng.read_kv(l, b, 0, int(lens[b])) for l in layers for b in (0, B - 1)]
+    ar, _ = eng.generate(prompts, T, 1)
+    assert np.array_equal(spec, ar)
+    kv_ar = [eng.read_kv(l, b, 0, int(lens[b])) for l in layers for b in (0, B - 1)]
+    for (k1, v1), (k2, v2) in zip(kv, kv_ar):
+        assert np.array_equal(k1, k2) and np.array_equal(v1, v2)
+    _say("ragged verify %s B=%d k_spec=%d (%d rows): %d steps, mean m %.2f"
+         % (name, B, k, B * k, info["steps"], info["m"].mean()))
+    eng.close()
+
+
 @pytest.mark.parametrize("name,r", [("tiny", 4), ("tiny", 6), ("tiny", 24), ("tiny", 64), ("1b_L4", 8),
                                     ("1b_L4", 20)])
 def test_draft_head_logits_at_other_lora_ranks(name, r):
